@@ -1,0 +1,520 @@
+/*
+ * NVFP4 ScaleSweep oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, single-threaded, deliberately slow CPU implementation of the ScaleSweep hot path
+ * (Lin & Wan, "ScaleSweep: Accurate NVFP4 Post-Training Quantization of LLMs via Block Scale
+ * Initialization", arXiv 2606.07618), written from the paper.  Only the tests, the smoke check
+ * and the benchmark's CPU-baseline leg load it; the product library neither links nor calls
+ * it, and the two share no code, header, table or generator.
+ *
+ * Precision.  The global scale S and the normalized values y = x / S are IEEE binary32 (C
+ * float division, round to nearest even).  Every objective value is computed in binary64.
+ * Build with -O2 -ffp-contract=off and without fast-math, so that no multiply-add is fused.
+ *
+ * Readings of points the paper leaves open are marked "reading:" where they are used; the
+ * design document lists all of them.  Every function here is pinned by the CPU test-suite
+ * (paper values, closed forms, invariants, brute force); none is "parity unpinned".
+ */
+#include "nvfp4_oracle.h"
+
+#include <float.h>
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define E2M1_CODES 8        /* non-negative E2M1 magnitudes, codes 0..7 */
+#define E4M3_MAX_CODE 126   /* codes 1..126 are the 126 positive finite E4M3 values */
+#define MAX_BLOCK 128
+
+/* ------------------------------------------------------------------------------------- */
+/* Number formats: Appendix A (floating-point representation).                            */
+/* ------------------------------------------------------------------------------------- */
+
+/* Value of the non-negative EeMm bit pattern code = a * 2^m + b (sign c = 0), with bias
+ * B = 2^(e-1) - 1:  a != 0 -> 2^(a-B) (1 + b / 2^m),  a == 0 -> 2^(1-B) b / 2^m.
+ * For a positive value the bit-pattern integer I(v) of Appendix A is the code itself. */
+double nvfp4_ref_eemm_value(int e, int m, int code)
+{
+    int bias = (1 << (e - 1)) - 1;
+    int a = code >> m;
+    int b = code & ((1 << m) - 1);
+    double mant = (double)(1 << m);
+    if (a != 0) return ldexp(1.0 + (double)b / mant, a - bias);
+    return ldexp((double)b / mant, 1 - bias);
+}
+
+static double g_e2m1[E2M1_CODES];
+static double g_e4m3[E4M3_MAX_CODE + 1];
+static int g_tables_ready = 0;
+
+static void tables_init(void)
+{
+    if (g_tables_ready) return;
+    for (int k = 0; k < E2M1_CODES; ++k) g_e2m1[k] = nvfp4_ref_eemm_value(2, 1, k);
+    for (int c = 0; c <= E4M3_MAX_CODE; ++c) g_e4m3[c] = nvfp4_ref_eemm_value(4, 3, c);
+    g_tables_ready = 1;
+}
+
+/* FP4 E2M1 magnitude of code k in 0..7: {0, 0.5, 1, 1.5, 2, 3, 4, 6} (NVFP4 section). */
+double nvfp4_ref_e2m1(int k)
+{
+    tables_init();
+    return (k >= 0 && k < E2M1_CODES) ? g_e2m1[k] : NAN;
+}
+
+/* FP8 E4M3 value of code c in 0..126; code 127 (exponent 15, mantissa 7) is NaN and is not a
+ * candidate: the paper counts 126 positive finite scales, the largest being 448. */
+double nvfp4_ref_e4m3(int c)
+{
+    tables_init();
+    return (c >= 0 && c <= E4M3_MAX_CODE) ? g_e4m3[c] : NAN;
+}
+
+/* ------------------------------------------------------------------------------------- */
+/* Rounding: Notation section (round to nearest / down onto a grid).                      */
+/* ------------------------------------------------------------------------------------- */
+
+/* Nearest point of the scaled grid FP4(s) = { s * v : v in G_FP4 } to a >= 0, returned as the
+ * E2M1 magnitude code.  a lies above the midpoint between codes k and k+1 exactly when the
+ * nearest point is past k.  reading: an exact midpoint goes to the even code (ties-to-even,
+ * as IEEE and OCP conversions do).  Each midpoint (v_k + v_{k+1}) / 2 * s has at most 7
+ * significant bits, so every comparison is exact.  FP4(0) = {0}. */
+int nvfp4_ref_round_fp4(double a, double s)
+{
+    if (s == 0.0) return 0;
+    int k = 0;
+    while (k < E2M1_CODES - 1) {
+        double mid = 0.5 * (nvfp4_ref_e2m1(k) + nvfp4_ref_e2m1(k + 1)) * s;
+        if (a > mid || (a == mid && ((k + 1) % 2) == 0))
+            k++;
+        else
+            break;
+    }
+    return k;
+}
+
+/* Round down onto the FP8 grid, of the ratio v_num / v_den (v_den in {4, 6}):
+ * the largest code c in 0..126 with v_den * E4M3(c) <= v_num.  The products are exact. */
+int nvfp4_ref_floor_fp8(double v_num, double v_den)
+{
+    int c = E4M3_MAX_CODE;
+    while (c > 0 && v_den * nvfp4_ref_e4m3(c) > v_num) c--;
+    return c;
+}
+
+/* Round to nearest onto the FP8 grid, of v_num / v_den.  reading: ties go to the even code
+ * and values beyond 448 saturate to 448 (code 126); the result may be code 0. */
+int nvfp4_ref_nearest_fp8(double v_num, double v_den)
+{
+    int c = nvfp4_ref_floor_fp8(v_num, v_den);
+    if (c < E4M3_MAX_CODE) {
+        double mid = 0.5 * v_den * (nvfp4_ref_e4m3(c) + nvfp4_ref_e4m3(c + 1));
+        if (v_num > mid || (v_num == mid && ((c + 1) % 2) == 0)) c++;
+    }
+    return c;
+}
+
+/* ------------------------------------------------------------------------------------- */
+/* Objective: Eq. (weighted_quantization_loss) and Eq. (mse_quantization_loss).          */
+/* ------------------------------------------------------------------------------------- */
+
+/* L(s; y, w) = sum_i w_i (y_i - round_FP4(s)(y_i))^2 over one micro-block of n normalized
+ * values (w == NULL: all w_i = 1).  The grid is symmetric, so the error of y_i equals that of
+ * |y_i|.  Terms are added in order i = 0 .. n-1 in binary64; the difference |y_i| - g s is
+ * exact in binary64 for every finite binary32 y_i the dynamic global scale can produce. */
+double nvfp4_ref_block_loss(const float* y, const float* w, int n, double s)
+{
+    double J = 0.0;
+    for (int i = 0; i < n; ++i) {
+        double a = fabs((double)y[i]);
+        double g = nvfp4_ref_e2m1(nvfp4_ref_round_fp4(a, s));
+        double e = a - g * s;
+        double t = e * e;
+        if (w) t = (double)w[i] * t;
+        J = J + t;
+    }
+    return J;
+}
+
+/* ------------------------------------------------------------------------------------- */
+/* Block scale selection: Method section (ScaleSweep, block scale bounds).               */
+/* ------------------------------------------------------------------------------------- */
+
+/* Offset of the lowest swept code below I(s_base^FP8).
+ *   MSE,  n = 16: 3 (Lemma 3: the argmin is >= 4/5 s_base^FP8, i.e. 3 codes down).
+ *   WMSE, n = 16: 8 (the empirical s_base / 2 bound).
+ *   reading for n > 16: MSE 5 / 7 / 11 for n = 32 / 64 / 128, from the r <= 3/4 step of the
+ *   proof of Lemma 3 with n - 1 non-maximal coordinates; WMSE max(8, MSE offset).
+ * AbsMax and 4/6 do not sweep (returns 0). */
+int nvfp4_ref_window_lower(int method, int n)
+{
+    int mse = (n == 16) ? 3 : (n == 32) ? 5 : (n == 64) ? 7 : (n == 128) ? 11 : -1;
+    if (mse < 0) return -1;
+    if (method == REF_SCALESWEEP_MSE) return mse;
+    if (method == REF_SCALESWEEP_WMSE) return mse > 8 ? mse : 8;
+    return 0;
+}
+
+/* Offset of the highest swept code above I(s_base^FP8): 7, from Lemma 1 (no scale above
+ * 12/7 s_base can beat its half) and Lemma 2 with alpha = 12/7 (Table 1). */
+int nvfp4_ref_window_upper(void) { return 7; }
+
+static double block_ymax(const float* y, int n)
+{
+    double m = 0.0;
+    for (int i = 0; i < n; ++i) {
+        double a = fabs((double)y[i]);
+        if (a > m) m = a;
+    }
+    return m;
+}
+
+/* ScaleSweep on one block: s_base = max|y| / 6, s_base^FP8 = round-down of s_base onto the
+ * FP8 grid, c0 = I(s_base^FP8); sweep codes [max(1, c0-L), min(126, c0+U)] and keep the
+ * argmin of L (reading: the smallest code wins a tie).  Also sweeps all 126 positive codes
+ * (the exhaustive search the window is meant to reproduce).  J127, if given, receives L at
+ * every code 0..126 (code 0 is the zero scale, whose loss is sum w y^2). */
+int nvfp4_ref_block_sweep(const float* y, const float* w, int n, int L, int U,
+                          int* c0_out, int* lo_out, int* hi_out, int* c_win, int* c_full,
+                          double* J127)
+{
+    double ymax = block_ymax(y, n);
+    int c0 = nvfp4_ref_floor_fp8(ymax, 6.0);
+    int lo = c0 - L < 1 ? 1 : c0 - L;
+    int hi = c0 + U > E4M3_MAX_CODE ? E4M3_MAX_CODE : c0 + U;
+    int best_w = -1, best_f = -1;
+    double jw = 0.0, jf = 0.0;
+    for (int c = 0; c <= E4M3_MAX_CODE; ++c) {
+        double J = nvfp4_ref_block_loss(y, w, n, nvfp4_ref_e4m3(c));
+        if (J127) J127[c] = J;
+        if (c == 0) continue;
+        if (best_f < 0 || J < jf) { best_f = c; jf = J; }
+        if (c >= lo && c <= hi && (best_w < 0 || J < jw)) { best_w = c; jw = J; }
+    }
+    if (c0_out) *c0_out = c0;
+    if (lo_out) *lo_out = lo;
+    if (hi_out) *hi_out = hi;
+    if (c_win) *c_win = best_w;
+    if (c_full) *c_full = best_f;
+    return REF_OK;
+}
+
+/* The scale code a method picks for one block of normalized values.
+ *   AbsMax (NVFP4 section): s = round-to-nearest-FP8(max|y| / 6).
+ *   4/6 (Introduction; Related Work): also try round-to-nearest-FP8(max|y| / 4), which maps the
+ *     block maximum to 4 instead of 6, and keep it only if its loss is strictly lower
+ *     (reading: loss as in the call -- weighted when weights are given -- ties keep /6).
+ *   ScaleSweep (Method section): argmin of L over the window only. */
+int nvfp4_ref_block_choose(int method, const float* y, const float* w, int n)
+{
+    double ymax = block_ymax(y, n);
+    if (method == REF_ABSMAX) return nvfp4_ref_nearest_fp8(ymax, 6.0);
+    if (method == REF_FOUR_OVER_SIX) {
+        int c6 = nvfp4_ref_nearest_fp8(ymax, 6.0);
+        int c4 = nvfp4_ref_nearest_fp8(ymax, 4.0);
+        double j6 = nvfp4_ref_block_loss(y, w, n, nvfp4_ref_e4m3(c6));
+        double j4 = nvfp4_ref_block_loss(y, w, n, nvfp4_ref_e4m3(c4));
+        return (j4 < j6) ? c4 : c6;
+    }
+    int L = nvfp4_ref_window_lower(method, n);
+    int U = nvfp4_ref_window_upper();
+    int c0 = nvfp4_ref_floor_fp8(ymax, 6.0);
+    int lo = c0 - L < 1 ? 1 : c0 - L;
+    int hi = c0 + U > E4M3_MAX_CODE ? E4M3_MAX_CODE : c0 + U;
+    const float* wm = (method == REF_SCALESWEEP_WMSE) ? w : NULL;
+    int best = lo;
+    double jb = nvfp4_ref_block_loss(y, wm, n, nvfp4_ref_e4m3(lo));
+    for (int c = lo + 1; c <= hi; ++c) {
+        double J = nvfp4_ref_block_loss(y, wm, n, nvfp4_ref_e4m3(c));
+        if (J < jb) { best = c; jb = J; }
+    }
+    return best;
+}
+
+/* ------------------------------------------------------------------------------------- */
+/* Tensor level: global scale (NVFP4 section; Global Scale Selection) and packing.        */
+/* ------------------------------------------------------------------------------------- */
+
+static float load_elem(const void* x, int dtype, int64_t i)
+{
+    if (dtype == 0) return ((const float*)x)[i];
+    uint32_t bits = (uint32_t)((const uint16_t*)x)[i] << 16;   /* bfloat16 -> binary32, exact */
+    float f;
+    memcpy(&f, &bits, sizeof f);
+    return f;
+}
+
+static int valid_block(int block)
+{
+    return block == 16 || block == 32 || block == 64 || block == 128;
+}
+
+static int valid_range(float d) { return isfinite(d) && d > 0.0f && d <= 448.0f; }
+
+/* S = amax / (6 D) in binary32 (D = 448 for AbsMax in the NVFP4 section, D = 256 for the
+ * global scale selection of ScaleSweep and 4/6).  reading: the denominator 6 D is formed in
+ * binary32 first; an all-zero tensor gets S = 1; a quotient that underflows to zero is raised
+ * to the smallest positive binary32 value.  A non-finite element is an error. */
+int nvfp4_ref_tensor_scale(const void* x, int dtype, int64_t count, float fp8_range, float* S)
+{
+    if (!S || (count > 0 && !x)) return REF_ERR_NULL;
+    if (dtype != 0 && dtype != 1) return REF_ERR_DTYPE;
+    if (count < 0) return REF_ERR_SHAPE;
+    if (!valid_range(fp8_range)) return REF_ERR_ARG;
+    float amax = 0.0f;
+    for (int64_t i = 0; i < count; ++i) {
+        float v = load_elem(x, dtype, i);
+        if (!isfinite(v)) return REF_ERR_NONFINITE;
+        float a = fabsf(v);
+        if (a > amax) amax = a;
+    }
+    if (amax == 0.0f) {
+        *S = 1.0f;
+        return REF_OK;
+    }
+    float denom = 6.0f * fp8_range;
+    float s = amax / denom;
+    if (s == 0.0f) s = FLT_TRUE_MIN;
+    *S = s;
+    return REF_OK;
+}
+
+int nvfp4_ref_quantize(int method, const void* x, int dtype, int64_t rows, int64_t cols,
+                       int block, float fp8_range, float static_scale, const float* col_weight,
+                       float* tensor_scale, uint8_t* q, uint8_t* scales)
+{
+    if (method < REF_ABSMAX || method > REF_SCALESWEEP_WMSE) return REF_ERR_ARG;
+    if (!tensor_scale) return REF_ERR_NULL;
+    if (dtype != 0 && dtype != 1) return REF_ERR_DTYPE;
+    if (!valid_block(block)) return REF_ERR_BLOCK;
+    if (rows < 0 || cols < 0 || cols % block != 0) return REF_ERR_SHAPE;
+    if (!valid_range(fp8_range)) return REF_ERR_ARG;
+    if (!isfinite(static_scale) || static_scale < 0.0f) return REF_ERR_ARG;
+    if (method == REF_SCALESWEEP_WMSE && !col_weight) return REF_ERR_NULL;
+    int64_t count = rows * cols;
+    if (count > 0 && (!x || !q || !scales)) return REF_ERR_NULL;
+    const float* w = (method == REF_SCALESWEEP_WMSE || method == REF_FOUR_OVER_SIX)
+                         ? col_weight : NULL;
+    if (w) {
+        for (int64_t j = 0; j < cols; ++j)
+            if (!isfinite(w[j]) || w[j] < 0.0f) return REF_ERR_ARG;
+    }
+
+    float S = static_scale;
+    if (S == 0.0f) {
+        int rc = nvfp4_ref_tensor_scale(x, dtype, count, fp8_range, &S);
+        if (rc != REF_OK) return rc;
+    }
+
+    int64_t nb_row = cols / block;
+    float y[MAX_BLOCK];
+    for (int64_t r = 0; r < rows; ++r) {
+        for (int64_t kb = 0; kb < nb_row; ++kb) {
+            int64_t base = r * cols + kb * block;
+            for (int i = 0; i < block; ++i) {
+                float v = load_elem(x, dtype, base + i);
+                y[i] = v / S;                        /* y = RN32(x / S) */
+                if (!isfinite(v) || !isfinite(y[i])) return REF_ERR_NONFINITE;
+            }
+            const float* wb = w ? w + kb * block : NULL;
+            int c = nvfp4_ref_block_choose(method, y, wb, block);
+            scales[r * nb_row + kb] = (uint8_t)c;
+            double s = nvfp4_ref_e4m3(c);
+            for (int i = 0; i < block; ++i) {
+                int k = nvfp4_ref_round_fp4(fabs((double)y[i]), s);
+                int nib = (signbit(y[i]) ? 8 : 0) | k;
+                int64_t e = base + i;
+                uint8_t* byte = &q[e >> 1];
+                if ((e & 1) == 0)
+                    *byte = (uint8_t)((*byte & 0xF0) | nib);
+                else
+                    *byte = (uint8_t)((*byte & 0x0F) | (nib << 4));
+            }
+        }
+    }
+    *tensor_scale = S;
+    return REF_OK;
+}
+
+int nvfp4_ref_quant_absmax(const void* x, int dtype, int64_t rows, int64_t cols, int block,
+                           float fp8_range, float static_scale, float* tensor_scale,
+                           uint8_t* q, uint8_t* scales)
+{
+    return nvfp4_ref_quantize(REF_ABSMAX, x, dtype, rows, cols, block, fp8_range,
+                              static_scale, NULL, tensor_scale, q, scales);
+}
+
+int nvfp4_ref_quant_four_over_six(const void* x, int dtype, int64_t rows, int64_t cols,
+                                  int block, float fp8_range, float static_scale,
+                                  const float* col_weight, float* tensor_scale, uint8_t* q,
+                                  uint8_t* scales)
+{
+    return nvfp4_ref_quantize(REF_FOUR_OVER_SIX, x, dtype, rows, cols, block, fp8_range,
+                              static_scale, col_weight, tensor_scale, q, scales);
+}
+
+int nvfp4_ref_quant_scalesweep_mse(const void* x, int dtype, int64_t rows, int64_t cols,
+                                   int block, float fp8_range, float static_scale,
+                                   float* tensor_scale, uint8_t* q, uint8_t* scales)
+{
+    return nvfp4_ref_quantize(REF_SCALESWEEP_MSE, x, dtype, rows, cols, block, fp8_range,
+                              static_scale, NULL, tensor_scale, q, scales);
+}
+
+int nvfp4_ref_quant_scalesweep_wmse(const void* x, int dtype, int64_t rows, int64_t cols,
+                                    int block, float fp8_range, float static_scale,
+                                    const float* col_weight, float* tensor_scale, uint8_t* q,
+                                    uint8_t* scales)
+{
+    return nvfp4_ref_quantize(REF_SCALESWEEP_WMSE, x, dtype, rows, cols, block, fp8_range,
+                              static_scale, col_weight, tensor_scale, q, scales);
+}
+
+/* Reconstruction x_hat_i = q_i * s_{block(i)} * S (NVFP4 section).  q * s is exact (at most 6
+ * significant bits); the product with S is formed exactly in binary64 and rounded once. */
+int nvfp4_ref_dequant(const uint8_t* q, const uint8_t* scales, float tensor_scale,
+                      int64_t rows, int64_t cols, int block, float* out)
+{
+    if (!valid_block(block)) return REF_ERR_BLOCK;
+    if (rows < 0 || cols < 0 || cols % block != 0) return REF_ERR_SHAPE;
+    if (rows * cols > 0 && (!q || !scales || !out)) return REF_ERR_NULL;
+    int64_t nb_row = cols / block;
+    for (int64_t r = 0; r < rows; ++r) {
+        for (int64_t j = 0; j < cols; ++j) {
+            int64_t e = r * cols + j;
+            int nib = (e & 1) ? (q[e >> 1] >> 4) : (q[e >> 1] & 15);
+            double v = nvfp4_ref_e2m1(nib & 7);
+            if (nib & 8) v = -v;
+            double qs = v * nvfp4_ref_e4m3(scales[r * nb_row + j / block]);
+            out[e] = (float)(qs * (double)tensor_scale);
+        }
+    }
+    return REF_OK;
+}
+
+/* ------------------------------------------------------------------------------------- */
+/* Appendix: optimal FP32 block scale, and its FP8-quantized version.                     */
+/* ------------------------------------------------------------------------------------- */
+
+static int cmp_double(const void* a, const void* b)
+{
+    double x = *(const double*)a, y = *(const double*)b;
+    return (x > y) - (x < y);
+}
+
+/* Loss of the block at a real scale s with the rounding index of each element held fixed at
+ * the one it takes at s_ref: the quadratic A - 2 B s + C s^2 of one segment. */
+static void segment_quadratic(const float* y, const float* w, int n, double s_ref, double* A,
+                              double* B, double* C)
+{
+    *A = *B = *C = 0.0;
+    for (int i = 0; i < n; ++i) {
+        double a = fabs((double)y[i]);
+        double wi = w ? (double)w[i] : 1.0;
+        double g = nvfp4_ref_e2m1(nvfp4_ref_round_fp4(a, s_ref));
+        *A += wi * a * a;
+        *B += wi * a * g;
+        *C += wi * g * g;
+    }
+}
+
+/* min over real s > 0 of L(s; y, w).  Each element's error is a piecewise quadratic in s
+ * whose breakpoints are the s at which |y_i| / s meets an FP4 midpoint; between consecutive
+ * breakpoints of the whole block the rounding indices are constant, so L is one quadratic
+ * there.  Enumerate the segments, minimize each quadratic on its closed segment, keep the
+ * least.  Returns the minimum; *s_opt receives the minimizer. */
+double nvfp4_ref_continuous_opt(const float* y, const float* w, int n, double* s_opt)
+{
+    double bp[7 * MAX_BLOCK + 2];
+    int nb = 0;
+    for (int i = 0; i < n; ++i) {
+        double a = fabs((double)y[i]);
+        if (a == 0.0) continue;
+        for (int k = 0; k < E2M1_CODES - 1; ++k) {
+            double mid = 0.5 * (nvfp4_ref_e2m1(k) + nvfp4_ref_e2m1(k + 1));
+            bp[nb++] = a / mid;
+        }
+    }
+    double A0 = 0.0;
+    for (int i = 0; i < n; ++i) {
+        double a = (double)y[i];
+        A0 += (w ? (double)w[i] : 1.0) * a * a;
+    }
+    double best = A0;           /* s -> infinity: everything rounds to zero */
+    double best_s = INFINITY;
+    if (nb == 0) {
+        if (s_opt) *s_opt = 1.0;
+        return 0.0;
+    }
+    qsort(bp, (size_t)nb, sizeof(double), cmp_double);
+    for (int seg = 0; seg <= nb; ++seg) {
+        double lo = (seg == 0) ? 0.0 : bp[seg - 1];
+        double hi = (seg == nb) ? INFINITY : bp[seg];
+        if (!(hi > lo)) continue;
+        double s_ref = (seg == 0) ? 0.5 * hi : (seg == nb) ? 2.0 * lo : 0.5 * (lo + hi);
+        double A, B, C;
+        segment_quadratic(y, w, n, s_ref, &A, &B, &C);
+        if (C <= 0.0) {
+            if (A < best) { best = A; best_s = s_ref; }
+            continue;
+        }
+        double s = B / C;
+        if (s < lo) s = lo;
+        if (s > hi) s = hi;
+        if (s <= 0.0) continue;
+        double val = A - 2.0 * B * s + C * s * s;
+        if (val < 0.0) val = 0.0;
+        if (val < best) { best = val; best_s = s; }
+    }
+    if (s_opt) *s_opt = best_s;
+    return best;
+}
+
+/* FP8-quantized optimal scale: the better (by L) of the FP8 values just below and just above
+ * the optimal real block scale, in the normalized domain y = x / S.  Returns the code. */
+int nvfp4_ref_fp8_quantized_opt(const float* y, const float* w, int n, double* loss)
+{
+    double s_opt;
+    nvfp4_ref_continuous_opt(y, w, n, &s_opt);
+    int cf = nvfp4_ref_floor_fp8(s_opt, 1.0);
+    int cc = cf;
+    if (nvfp4_ref_e4m3(cf) < s_opt && cf < E4M3_MAX_CODE) cc = cf + 1;
+    if (cf < 1) cf = 1;
+    if (cc < 1) cc = 1;
+    double jf = nvfp4_ref_block_loss(y, w, n, nvfp4_ref_e4m3(cf));
+    double jc = nvfp4_ref_block_loss(y, w, n, nvfp4_ref_e4m3(cc));
+    int c = (jc < jf) ? cc : cf;
+    if (loss) *loss = (jc < jf) ? jc : jf;
+    return c;
+}
+
+/* ------------------------------------------------------------------------------------- */
+/* Metrics: Notation section.                                                             */
+/* ------------------------------------------------------------------------------------- */
+
+/* MSE = |x - xh|^2 / N, NMSE = |x - xh|^2 / |x|^2, WMSE = sum w (x - xh)^2 / sum w,
+ * NWMSE = sum w (x - xh)^2 / sum w x^2, with the per-column weight broadcast over rows. */
+int nvfp4_ref_metrics(const void* x, int dtype, const float* xhat, int64_t rows, int64_t cols,
+                      const float* col_weight, double* out4)
+{
+    if (!out4 || (rows * cols > 0 && (!x || !xhat))) return REF_ERR_NULL;
+    double se = 0.0, sx = 0.0, wse = 0.0, wsx = 0.0, sw = 0.0;
+    for (int64_t r = 0; r < rows; ++r) {
+        for (int64_t j = 0; j < cols; ++j) {
+            double v = (double)load_elem(x, dtype, r * cols + j);
+            double d = v - (double)xhat[r * cols + j];
+            double wj = col_weight ? (double)col_weight[j] : 1.0;
+            se += d * d;
+            sx += v * v;
+            wse += wj * d * d;
+            wsx += wj * v * v;
+            sw += wj;
+        }
+    }
+    double N = (double)(rows * cols);
+    out4[0] = N > 0 ? se / N : 0.0;
+    out4[1] = sx > 0 ? se / sx : 0.0;
+    out4[2] = sw > 0 ? wse / sw : 0.0;
+    out4[3] = wsx > 0 ? wse / wsx : 0.0;
+    return REF_OK;
+}

@@ -1,0 +1,66 @@
+"""Planted mistakes: each test builds a copy of the oracle with one plausible bug and checks
+that the CPU pin suite catches it.  The mistakes are planted in the oracle only, on the CPU."""
+import os
+import subprocess
+import sys
+from pathlib import Path
+
+import pytest
+
+import oracle
+
+ROOT = Path(__file__).resolve().parents[1]
+
+# (name, original text, planted text): every original must occur exactly once.
+MUTANTS = [
+    ("fp4_tie_rule", "if (a > mid || (a == mid && ((k + 1) % 2) == 0))",
+     "if (a > mid || (a == mid && ((k + 1) % 2) == 1))"),
+    ("fp8_tie_rule", "if (v_num > mid || (v_num == mid && ((c + 1) % 2) == 0)) c++;",
+     "if (v_num > mid || (v_num == mid && ((c + 1) % 2) == 1)) c++;"),
+    ("window_upper_6", "int nvfp4_ref_window_upper(void) { return 7; }",
+     "int nvfp4_ref_window_upper(void) { return 6; }"),
+    ("mse_lower_2", "int mse = (n == 16) ? 3 :", "int mse = (n == 16) ? 2 :"),
+    ("wmse_lower_7", "return mse > 8 ? mse : 8;", "return mse > 7 ? mse : 7;"),
+    ("weight_dropped", "if (w) t = (double)w[i] * t;", "if (0) t = (double)w[i] * t;"),
+    ("abs_error_not_squared", "double t = e * e;", "double t = fabs(e);"),
+    ("eemm_bias_off_by_one", "int bias = (1 << (e - 1)) - 1;", "int bias = (1 << (e - 1));"),
+    ("fp8_floor_strictness", "while (c > 0 && v_den * nvfp4_ref_e4m3(c) > v_num) c--;",
+     "while (c > 0 && v_den * nvfp4_ref_e4m3(c) >= v_num) c--;"),
+    ("argmin_tie_largest_code", "if (J < jb) { best = c; jb = J; }",
+     "if (J <= jb) { best = c; jb = J; }"),
+    ("sign_dropped", "int nib = (signbit(y[i]) ? 8 : 0) | k;", "int nib = k;"),
+    ("dequant_nibble_order", "int nib = (e & 1) ? (q[e >> 1] >> 4) : (q[e >> 1] & 15);",
+     "int nib = (e & 1) ? (q[e >> 1] & 15) : (q[e >> 1] >> 4);"),
+    ("global_scale_uses_4", "float denom = 6.0f * fp8_range;", "float denom = 4.0f * fp8_range;"),
+    ("four_over_six_tie_to_4", "return (j4 < j6) ? c4 : c6;", "return (j4 <= j6) ? c4 : c6;"),
+    ("four_over_six_uses_3", "int c4 = nvfp4_ref_nearest_fp8(ymax, 4.0);",
+     "int c4 = nvfp4_ref_nearest_fp8(ymax, 3.0);"),
+    ("normalize_by_reciprocal", "y[i] = v / S;", "y[i] = v * (1.0f / S);"),
+    ("s0_rounds_to_nearest_in_choose",
+     "int U = nvfp4_ref_window_upper();\n    int c0 = nvfp4_ref_floor_fp8(ymax, 6.0);",
+     "int U = nvfp4_ref_window_upper();\n    int c0 = nvfp4_ref_nearest_fp8(ymax, 6.0);"),
+    ("s0_rounds_to_nearest_in_sweep",
+     "double ymax = block_ymax(y, n);\n    int c0 = nvfp4_ref_floor_fp8(ymax, 6.0);",
+     "double ymax = block_ymax(y, n);\n    int c0 = nvfp4_ref_nearest_fp8(ymax, 6.0);"),
+    ("window_not_clamped_to_1", "int lo = c0 - L < 1 ? 1 : c0 - L;\n    int hi = c0 + U > E4M3_MAX_CODE ? E4M3_MAX_CODE : c0 + U;\n    const float* wm",
+     "int lo = c0 - L < 0 ? 0 : c0 - L;\n    int hi = c0 + U > E4M3_MAX_CODE ? E4M3_MAX_CODE : c0 + U;\n    const float* wm"),
+    ("zero_tensor_scale", "        *S = 1.0f;\n        return REF_OK;", "        *S = 0.5f;\n        return REF_OK;"),
+]
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name,orig,planted", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_planted_mistake_is_caught(name, orig, planted, tmp_path):
+    src = oracle.SRC.read_text()
+    assert src.count(orig) == 1, f"anchor for {name} must occur exactly once"
+    (tmp_path / "nvfp4_oracle.c").write_text(src.replace(orig, planted))
+    (tmp_path / "nvfp4_oracle.h").write_text((oracle.HERE / "nvfp4_oracle.h").read_text())
+    lib = tmp_path / "libmutant.so"
+    subprocess.run(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fPIC", "-shared", "-o",
+                    str(lib), str(tmp_path / "nvfp4_oracle.c"), "-lm"], check=True)
+    env = dict(os.environ, NVFP4_ORACLE_LIB=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        "-m", "not slow", "tests/test_oracle_pins.py",
+                        "tests/test_oracle_bruteforce.py"],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"planted mistake {name} was not caught:\n{r.stdout[-2000:]}"
