@@ -12,6 +12,10 @@ import oracle
 ROOT = Path(__file__).resolve().parents[1]
 
 # (name, original text, planted text): every original must occur exactly once.
+# Not listed: rounding s_base to the nearest instead of down inside the selection only.  It
+# moves the window up by one code exactly when max|y| / 6 lies above an FP8 midpoint; the
+# extra top code then ties at best with I(s_base^FP8) (Lemma 1), and no block with an optimum
+# at the lower edge and such a maximum was found, so its outputs match the oracle's.
 MUTANTS = [
     ("fp4_tie_rule", "if (a > mid || (a == mid && ((k + 1) % 2) == 0))",
      "if (a > mid || (a == mid && ((k + 1) % 2) == 1))"),
@@ -36,9 +40,6 @@ MUTANTS = [
     ("four_over_six_uses_3", "int c4 = nvfp4_ref_nearest_fp8(ymax, 4.0);",
      "int c4 = nvfp4_ref_nearest_fp8(ymax, 3.0);"),
     ("normalize_by_reciprocal", "y[i] = v / S;", "y[i] = v * (1.0f / S);"),
-    ("s0_rounds_to_nearest_in_choose",
-     "int U = nvfp4_ref_window_upper();\n    int c0 = nvfp4_ref_floor_fp8(ymax, 6.0);",
-     "int U = nvfp4_ref_window_upper();\n    int c0 = nvfp4_ref_nearest_fp8(ymax, 6.0);"),
     ("s0_rounds_to_nearest_in_sweep",
      "double ymax = block_ymax(y, n);\n    int c0 = nvfp4_ref_floor_fp8(ymax, 6.0);",
      "double ymax = block_ymax(y, n);\n    int c0 = nvfp4_ref_nearest_fp8(ymax, 6.0);"),
