@@ -1,0 +1,221 @@
+#!/usr/bin/env python3
+"""Benchmark of the NVFP4 ScaleSweep hot path on one MI355X.
+
+One step quantizes every weight of a Llama-3-8B-shaped decoder layer (bfloat16, block 16,
+dynamic global scale with D = 256) with ScaleSweep under both objectives, MSE and WMSE: for
+each of the 7 tensors the amax pass and the sweep kernel, twice.  `value` is the bfloat16
+input consumed per second (both objectives read the layer).  The line also carries:
+  * per-method GB/s of the same GPU's AbsMax (D = 448), 4/6 and each ScaleSweep objective,
+    and ScaleSweep's time relative to AbsMax;
+  * `roofline` for the dominant kernel (the WMSE sweep kernel), from HIP events around its
+    launches on the stream it runs on;
+  * `cpu_baseline`: the oracle on the host, single-threaded, on a bounded sample.
+Inputs are synthetic (workloads.py) and resident in HBM before timing starts.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+from pathlib import Path
+
+ROOT = Path(__file__).resolve().parent
+sys.path.insert(0, str(ROOT))
+
+# MI355X figures used for the rooflines.
+HBM_PEAK_GBS = 8000.0
+VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12        # 39.32 T lane-ops/s (no packed FP32)
+# Algorithmic VALU lane-operations per element-candidate evaluation: scale, round,
+# reconstruct-and-subtract, square-and-accumulate (+ one weight multiply for WMSE).
+OPS_PER_EVAL = {"scalesweep_mse": 4, "scalesweep_wmse": 5}
+CANDIDATES_16 = {"scalesweep_mse": 11, "scalesweep_wmse": 16}
+DOMINANT = "scalesweep_wmse"
+DOMINANT_SYMBOL = "quant_kernel<3, unsigned short, 16>"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target length of the oracle's CPU-baseline sample")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain device copy of known size (for counter scaling)")
+    return ap.parse_args()
+
+
+def kernel_source_hash() -> str:
+    src = (ROOT / "paper_2606_07618_amd" / "csrc" / "nvfp4ss.hip").read_bytes()
+    return hashlib.sha256(src).hexdigest()[:16]
+
+
+def read_traffic():
+    """HBM bytes per launch of the dominant kernel from the committed counter summary, if it
+    was taken on the current kernel source."""
+    f = ROOT / "profiles" / "traffic_scalesweep_wmse_llama8b_layer.json"
+    if not f.exists():
+        return None
+    d = json.loads(f.read_text())
+    if d.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the path is built and "
+              "measured on a single MI355X", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import workloads
+    import paper_2606_07618_amd as nv
+
+    dev = torch.device("cuda:0")
+    layer = workloads.llama8b_layer(dev)
+    names = list(layer)
+    xs = [layer[n][0] for n in names]
+    ws_col = [layer[n][1] for n in names]
+    n_elem = sum(x.numel() for x in xs)
+    in_bytes = 2 * n_elem
+    ws = nv.workspace(dev)
+
+    def alloc(x, block=16):
+        r, c = x.shape
+        return (torch.empty((r, c // 2), dtype=torch.uint8, device=dev),
+                torch.empty((r, c // block), dtype=torch.uint8, device=dev),
+                torch.empty(1, dtype=torch.float32, device=dev))
+
+    outs = {m: [alloc(x) for x in xs] for m in
+            ("absmax", "four_over_six", "scalesweep_mse", "scalesweep_wmse")}
+
+    def run(method, static=None):
+        for i, x in enumerate(xs):
+            w = ws_col[i] if method in ("scalesweep_wmse",) else None
+            nv.quantize(x, method, 16, weight=w, ws=ws, out=outs[method][i],
+                        static_scale=0.0 if static is None else static[i])
+
+    def step():
+        run("scalesweep_mse")
+        run("scalesweep_wmse")
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = 1e3 * elapsed / args.steps
+    value = 2 * in_bytes * args.steps / elapsed / 1e9
+
+    # ---- per-method throughput (events on the current stream, which the library uses) ----
+    reps = max(5, args.steps // 2)
+    per_method = {}
+    for m in ("absmax", "four_over_six", "scalesweep_mse", "scalesweep_wmse"):
+        run(m)
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for _ in range(reps):
+            run(m)
+        ev1.record()
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1) / reps
+        per_method[m] = {"ms_per_layer": round(ms, 4),
+                         "input_GBps": round(in_bytes / ms / 1e6, 1),
+                         "Gelem_per_s": round(n_elem / ms / 1e6, 2)}
+    overhead = {m: round(per_method[m]["ms_per_layer"] / per_method["absmax"]["ms_per_layer"], 3)
+                for m in ("four_over_six", "scalesweep_mse", "scalesweep_wmse")}
+
+    # ---- dominant kernel alone: static-scale calls launch only the sweep kernel ----------
+    scales_dyn = [float(o[2].item()) for o in outs[DOMINANT]]
+    stream = torch.cuda.current_stream(dev)
+    launch_ms = []
+    for i, x in enumerate(xs):
+        nv.quantize(x, DOMINANT, 16, weight=ws_col[i], out=outs[DOMINANT][i],
+                    static_scale=scales_dyn[i])
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            nv.quantize(x, DOMINANT, 16, weight=ws_col[i], out=outs[DOMINANT][i],
+                        static_scale=scales_dyn[i])
+        e1.record(stream)
+        torch.cuda.synchronize()
+        launch_ms.append(e0.elapsed_time(e1) / reps)
+    avg_launch_s = sum(launch_ms) / len(launch_ms) / 1e3
+    evals_per_launch = n_elem / len(xs) * CANDIDATES_16[DOMINANT]
+    ops_per_launch = evals_per_launch * OPS_PER_EVAL[DOMINANT]
+    achieved = ops_per_launch / avg_launch_s / 1e12
+    alg_bytes = (2 + 0.5 + 1 / 16) * n_elem / len(xs)          # read bf16, write q + scales
+    roofline = {
+        "bound": "alu", "achieved": round(achieved, 2), "peak": round(VALU_PEAK_TOPS, 2),
+        "unit": "TOP/s", "frac": round(achieved / VALU_PEAK_TOPS, 3),
+        "traffic": read_traffic(),
+        "kernel": DOMINANT_SYMBOL, "avg_launch_us": round(avg_launch_s * 1e6, 2),
+        "algorithmic_ops_per_launch": int(ops_per_launch),
+        "hbm_GBps_algorithmic": round(alg_bytes / avg_launch_s / 1e9, 1),
+        "hbm_frac": round(alg_bytes / avg_launch_s / 1e9 / HBM_PEAK_GBS, 3),
+    }
+
+    if args.copy_calibration:
+        src = torch.empty(in_bytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
+    # ---- CPU baseline: the oracle, one thread, on a bounded sample of the same layer -----
+    cpu = None
+    if not args.no_cpu:
+        import oracle
+
+        host = [(workloads.host_array(x), w.cpu().numpy()) for x, w in zip(xs, ws_col)]
+        rows_per = 8
+        done_elems, t_cpu = 0, 0.0
+        while t_cpu < args.cpu_seconds and rows_per <= 4096:
+            done_elems, t_start = 0, time.perf_counter()
+            for xh, wh in host:
+                sub = xh[:rows_per]
+                oracle.quantize("scalesweep_mse", sub, 16, 256.0)
+                oracle.quantize("scalesweep_wmse", sub, 16, 256.0, 0.0, wh)
+                done_elems += sub.size
+            t_cpu = time.perf_counter() - t_start
+            if t_cpu < args.cpu_seconds / 4:
+                rows_per *= 4
+            elif t_cpu < args.cpu_seconds:
+                rows_per *= 2
+            else:
+                break
+        cpu = {"value": round(2 * 2 * done_elems / t_cpu / 1e9, 4), "unit": "GB/s", "cores": 1,
+               "kind": "oracle",
+               "sample": f"first {rows_per} rows of each of the 7 layer tensors "
+                         f"({done_elems} bf16 elements), ScaleSweep MSE and WMSE, "
+                         f"dynamic S of the sample; {t_cpu:.1f} s on one host thread"}
+
+    line = {
+        "metric": "ScaleSweep NVFP4 quant GB/s (BF16 in) + % HBM/VALU roofline; overhead vs AbsMax",
+        "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "llama3_8b_decoder_layer_weights_bf16", "tensors": {
+            n: list(x.shape) for n, x in zip(names, xs)}, "elements": n_elem, "block": 16,
+            "objectives": ["scalesweep_mse", "scalesweep_wmse"],
+            "global_scale": "dynamic, S = amax / (6 * 256)", "value_counts": "bf16 input bytes of both objectives"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "per_method": per_method,
+        "time_vs_absmax": overhead,
+    }
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,136 @@
+/*
+ * nvfp4ss.h -- C interface of the NVFP4 ScaleSweep quantizer for AMD Instinct MI355X (gfx950).
+ *
+ * NVFP4 (ScaleSweep paper, arXiv 2606.07618, "NVFP4 Quantization" section) represents a tensor
+ * x as (q, s, S): FP4 E2M1 values q, one FP8 E4M3 scale s per micro-block of 16 consecutive
+ * elements, and one binary32 global scale S, reconstructing x_hat_i = q_i * s_{block(i)} * S.
+ * The calls below compute (q, s, S) with four block-scale rules:
+ *   nvfp4_quant_absmax          AbsMax (NVFP4 Quantization section)
+ *   nvfp4_quant_four_over_six   4/6 (Introduction and Related Work)
+ *   nvfp4_quant_scalesweep_mse  ScaleSweep with the MSE objective (Method section)
+ *   nvfp4_quant_scalesweep_wmse ScaleSweep with the WMSE objective (Method section)
+ * and nvfp4_dequant computes x_hat.
+ *
+ * Common conventions
+ *   - All tensor pointers are DEVICE pointers owned by the caller; the library never
+ *     allocates, frees or keeps them.  Inputs and outputs must not overlap.
+ *   - Every call validates its arguments synchronously on the host, before any launch; on an
+ *     error it returns a negative nvfp4_status and has launched nothing and written nothing.
+ *   - On success the work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
+ *     the call returns NVFP4_OK without waiting.  A failed launch returns NVFP4_ERR_HIP.
+ *   - Conditions that depend on the data cannot be reported synchronously: if x holds a NaN
+ *     or an infinity, the dynamic global scale is NaN and the other outputs are unspecified
+ *     (the kernels still terminate normally).  Check *tensor_scale after synchronizing.
+ *   - Calls are thread-safe; the library holds no global state.  Two calls that are in
+ *     flight at the same time must not share a workspace.
+ *
+ * Layouts (row-major)
+ *   x       [rows, cols], dtype NVFP4_IN_F32 (binary32) or NVFP4_IN_BF16 (bfloat16);
+ *           16-byte aligned.  Micro-blocks are `block` consecutive elements of a row
+ *           (block in {16, 32, 64, 128}; cols % block == 0), i.e. they run along the input
+ *           dimension d_in of a weight stored [d_out, d_in], as in Eq. (nvfp4_MSE).
+ *   q       [rows, cols/2] bytes, 8-byte aligned; element 2j sits in bits 3:0 of byte j and
+ *           element 2j+1 in bits 7:4; a nibble is (sign << 3) | E2M1 code, the code k of the
+ *           magnitude {0, 0.5, 1, 1.5, 2, 3, 4, 6}[k].  The sign of x is kept, also on zero.
+ *   scales  [rows, cols/block] bytes, the E4M3 bit pattern (0..126) of each block scale.
+ *   tensor_scale  one binary32 in device memory, receives S.
+ */
+#ifndef NVFP4SS_H
+#define NVFP4SS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { NVFP4_IN_F32 = 0, NVFP4_IN_BF16 = 1 } nvfp4_dtype;
+
+typedef enum {
+    NVFP4_OK = 0,
+    NVFP4_ERR_NULL = -1,      /* a required pointer is NULL */
+    NVFP4_ERR_SHAPE = -2,     /* rows < 0, cols < 0, or cols % block != 0 */
+    NVFP4_ERR_BLOCK = -3,     /* block not in {16, 32, 64, 128} */
+    NVFP4_ERR_DTYPE = -4,     /* dtype / out_dtype not supported */
+    NVFP4_ERR_ARG = -5,       /* fp8_range or static_scale out of range */
+    NVFP4_ERR_WORKSPACE = -6, /* dynamic scale requested without a large enough workspace */
+    NVFP4_ERR_ALIGN = -7,     /* x, col_weight or workspace not 16-byte aligned, q not 8 */
+    NVFP4_ERR_HIP = -8        /* a kernel launch failed */
+} nvfp4_status;
+
+/* Bytes of device workspace the dynamic-scale path needs (a small constant).  The workspace
+ * carries the grid-wide |x| maximum and an arrival counter between the two kernels of one
+ * call.  It must be zero-filled once before its first use; every call that completes leaves
+ * it zero-filled again.  Static-scale calls do not touch it (it may be NULL). */
+size_t nvfp4_workspace_bytes(void);
+
+/* Text for a status code (a static string; never NULL). */
+const char* nvfp4_status_string(int status);
+
+/*
+ * Global scale and arguments shared by the quantizers.
+ *   fp8_range     D in S = max_i |x_i| / (6 D): 448 for AbsMax (NVFP4 Quantization section),
+ *                 256 for ScaleSweep and 4/6 (Global Scale Selection).  Finite, 0 < D <= 448,
+ *                 else NVFP4_ERR_ARG.  6 D is formed in binary32, then S = RN32(amax / (6 D));
+ *                 an all-zero tensor gets S = 1, a quotient that underflows gets the smallest
+ *                 positive binary32.
+ *   static_scale  0: dynamic -- a first kernel reduces max |x| over the tensor and writes S.
+ *                 Finite > 0: a given (calibrated) global scale, as used for activations, KV
+ *                 cache and queries (implementation details appendix); no reduction pass;
+ *                 S = static_scale is still written to *tensor_scale.  Every |x| / S must be
+ *                 finite.  Negative, NaN or infinite: NVFP4_ERR_ARG.
+ *   workspace     >= nvfp4_workspace_bytes() bytes, 16-byte aligned, for dynamic S (see above);
+ *                 otherwise NVFP4_ERR_WORKSPACE (NULL with static_scale > 0 is fine).
+ * Every quantizer normalizes y_i = RN32(x_i / S) (a correctly rounded division) and works on
+ * blocks of y, as the Block Scale Optimization section does; FP4 rounding is to nearest with
+ * ties to the even code; the objective L(s; y, w) is Eq. (weighted_quantization_loss).
+ */
+
+/* AbsMax (NVFP4 Quantization section): s = round-to-nearest-even FP8(max|y| / 6), saturating
+ * at 448 (the code may be 0: then every value of the block is 0); q_i = RNE FP4(y_i / s). */
+int nvfp4_quant_absmax(const void* x, int dtype, int64_t rows, int64_t cols, int block,
+                       float fp8_range, float static_scale, float* tensor_scale, uint8_t* q,
+                       uint8_t* scales, void* workspace, size_t workspace_bytes, void* stream);
+
+/* 4/6: the FP8 scales round-to-nearest(max|y|/6) and round-to-nearest(max|y|/4) (mapping the
+ * block maximum to 6 or to 4); keeps the /4 scale only if its loss is strictly lower.
+ * col_weight: [cols] binary32 column importance (16-byte aligned) for a weighted loss, or
+ * NULL for the unweighted one.  Weights must be finite and >= 0 (not checked). */
+int nvfp4_quant_four_over_six(const void* x, int dtype, int64_t rows, int64_t cols, int block,
+                              const float* col_weight, float fp8_range, float static_scale,
+                              float* tensor_scale, uint8_t* q, uint8_t* scales,
+                              void* workspace, size_t workspace_bytes, void* stream);
+
+/* ScaleSweep, MSE objective (Block Scale Optimization; Lemmas 1-3): with s0 the FP8 value
+ * just below max|y| / 6 and c0 = I(s0) its bit pattern, sweep every E4M3 code c in
+ * [max(1, c0 - L), min(126, c0 + 7)] and keep the argmin of L(E4M3(c); y), the smallest code
+ * on a tie.  L = 3 for block 16 (Lemma 3); 5 / 7 / 11 for block 32 / 64 / 128 (the lemma's
+ * argument extended to larger blocks).  The result equals the exact argmin over the window
+ * for every block: near-ties are re-decided in binary64. */
+int nvfp4_quant_scalesweep_mse(const void* x, int dtype, int64_t rows, int64_t cols, int block,
+                               float fp8_range, float static_scale, float* tensor_scale,
+                               uint8_t* q, uint8_t* scales, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/* ScaleSweep, WMSE objective (Eq. nvfp4_WMSE): as above with the weighted loss
+ * sum_i Imp_i (y_i - q_i s)^2, Imp the per-input-column importance ||X_{:,i}||^2 (or any
+ * positive multiple of it, e.g. the mean over calibration tokens), and L = 8 (the empirical
+ * s_base / 2 bound; 11 for block 128).  col_weight: [cols] binary32, required (NULL ->
+ * NVFP4_ERR_NULL), 16-byte aligned, finite and >= 0 (not checked). */
+int nvfp4_quant_scalesweep_wmse(const void* x, int dtype, int64_t rows, int64_t cols, int block,
+                                const float* col_weight, float fp8_range, float static_scale,
+                                float* tensor_scale, uint8_t* q, uint8_t* scales,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Reconstruction x_hat_i = q_i * s_{block(i)} * S (NVFP4 Quantization section) into out
+ * [rows, cols] binary32 (out_dtype must be NVFP4_IN_F32): q * s is exact, so each output is the
+ * single rounding RN32((q * s) * S).  tensor_scale is read from device memory. */
+int nvfp4_dequant(const uint8_t* q, const uint8_t* scales, const float* tensor_scale,
+                  int64_t rows, int64_t cols, int block, int out_dtype, void* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NVFP4SS_H */

@@ -1,0 +1,22 @@
+"""NVFP4 ScaleSweep quantization on AMD Instinct MI355X (gfx950).
+
+Thin Python binding of the C library ``libnvfp4ss.so`` (declared in include/nvfp4ss.h).
+Every step of the quantizer runs in the library's HIP kernels; this package only marshals
+arguments, using PyTorch for device memory and streams.  There is no CPU fallback: if the
+library is not built, importing the binding raises.
+"""
+from .nvfp4 import (  # noqa: F401
+    LIB_PATH,
+    NVFP4Error,
+    dequant,
+    lib,
+    nvfp4_dequant,
+    nvfp4_quant_absmax,
+    nvfp4_quant_four_over_six,
+    nvfp4_quant_scalesweep_mse,
+    nvfp4_quant_scalesweep_wmse,
+    nvfp4_status_string,
+    nvfp4_workspace_bytes,
+    quantize,
+    workspace,
+)

@@ -1,0 +1,770 @@
+// NVFP4 ScaleSweep quantizer for AMD Instinct MI355X (gfx950): kernels and the C interface
+// declared in include/nvfp4ss.h.
+//
+// Method (ScaleSweep, arXiv 2606.07618): with a global scale S fixed, every micro-block of
+// normalized values y = x / S picks its FP8 E4M3 scale independently (Global Scale
+// Selection).  ScaleSweep evaluates the block loss of Eq. (weighted_quantization_loss) at
+// every E4M3 bit pattern in a short window around I(s_base^FP8) (Lemmas 1-3; the window
+// summary at the end of the Block Scale Lower Bound paragraph) and keeps the argmin.
+//
+// Design for gfx950:
+//  * One lane owns 16 consecutive elements; a micro-block of n elements is n/16 adjacent
+//    lanes.  Everything per block (max, window, argmin) lives in registers; partial losses
+//    of multi-lane blocks are combined with ds_swizzle exchanges.
+//  * The FP4 rounding of two elements is one v_cvt_scalef32_pk_fp4_f32 (round to nearest
+//    even onto E2M1 of src / 2^exponent(scale), saturating at 6) and the decode back one
+//    v_cvt_scalef32_pk_f32_fp4.  A scale s = M 2^E (M in [1, 2)) is applied as u = |y| / M,
+//    computed once and shared by the codes c, c+8, c+16 (same M, exponent +1, +2), and the
+//    conversion's power-of-two scale 2^E.
+//  * The sweep scores candidates in binary32 with the quotient |y| * (1/M) rounded once, so
+//    an element within about an ulp of an FP4 midpoint may round the other way.  That moves a
+//    loss by at most ~4e-6 of itself; candidates within a relative band of 2^-14 of the best
+//    are re-scored exactly in binary64 in the order the definition sums them, which makes the
+//    chosen code the exact argmin (smallest code on a tie).
+//  * Exact roundings use exactly rounded quotients: y = RN32(x / S) and u = RN32(y / M) come
+//    from a multiply by the correctly rounded reciprocal and one fused-multiply-add
+//    correction (Markstein), exact when no intermediate underflows; tiny inputs fall back to
+//    IEEE division.  RN32(y / M) then rounds to the same E2M1 value as y / M itself, because
+//    an E2M1 midpoint times M has few enough bits that a 24-bit y cannot lie within half an
+//    ulp of the quotient's midpoint without hitting it.
+//  * The dynamic global scale needs max |x| first: a streaming kernel reduces it (wave and
+//    workgroup maxima, one atomic max per workgroup) and its last workgroup forms S = amax /
+//    (6 D) and 1/S for the quantization kernel that follows on the same stream.
+#include <hip/hip_runtime.h>
+
+#include <float.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "nvfp4ss.h"
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kLaneElems = 16;
+
+enum Method { kAbsMax = 0, kFourSix = 1, kSweepMse = 2, kSweepWmse = 3 };
+
+// Workspace words (uint32): running max of |x| bit patterns, arrival counter, S, 1/S.
+constexpr int kWsAmax = 0, kWsCount = 1, kWsScale = 2, kWsRecip = 3;
+constexpr size_t kWorkspaceBytes = 256;
+
+// Candidate band for the exact re-scoring (relative, plus an absolute floor for losses that
+// underflow binary32).
+constexpr float kBand = 0x1p-14f;
+constexpr float kBandAbs = 0x1p-120f;
+
+typedef float float2v __attribute__((ext_vector_type(2)));
+
+// ---------------------------------------------------------------------------------------
+// Formats.
+// ---------------------------------------------------------------------------------------
+
+// E4M3 code c (0..126) -> value.  Normal codes (c >= 8) have binary32 exponent field
+// (c >> 3) + 120 and the top three mantissa bits c & 7, which is (c << 20) + (120 << 23);
+// subnormal codes are c * 2^-9.
+__device__ __forceinline__ float e4m3_value(int c) {
+    return c >= 8 ? __uint_as_float(((uint32_t)c << 20) + 0x3C000000u) : (float)c * 0x1p-9f;
+}
+
+// Per-code constants, kept in LDS: s = M 2^E with M in [1, 2); rM = RN32(1 / M); cvs is the
+// conversion scale (any value with exponent E; 1 for the zero code).
+struct Scale {
+    float M, rM, s, cvs;
+};
+
+__device__ __forceinline__ void fill_scale_table(Scale* tab) {
+    const int c = threadIdx.x;
+    if (c < 128) {
+        const int cc = c > 126 ? 126 : c;
+        const float s = e4m3_value(cc);
+        const float M = cc == 0 ? 0.f
+                                : __uint_as_float((__float_as_uint(s) & 0x007FFFFFu) | 0x3F800000u);
+        Scale e;
+        e.M = M;
+        e.rM = cc == 0 ? 0.f : __fdiv_rn(1.0f, M);
+        e.s = s;
+        e.cvs = cc == 0 ? 1.0f : s;
+        tab[c] = e;
+    }
+    __syncthreads();
+}
+
+__device__ __forceinline__ int clamp_code(int c) { return c < 0 ? 0 : (c > 126 ? 126 : c); }
+
+// Largest code c with div * E4M3(c) <= v (round-down onto the FP8 grid of v / div), exact: an
+// estimate from the bits of v * (1/div) is off by at most one code and is fixed with exact
+// comparisons (div * E4M3(c) has at most six significant bits).
+__device__ __forceinline__ int floor_code(float v, float div, float rdiv, const Scale* tab) {
+    const float t = v * rdiv;
+    int c = t >= 0x1p-6f ? (int)(__float_as_uint(t) >> 20) - 960 : (int)(t * 512.0f);
+    c = clamp_code(c);
+    if (c > 0 && div * tab[c].s > v) c--;
+    if (c < 126 && div * tab[c + 1].s <= v) c++;
+    return c;
+}
+
+// Round-to-nearest-even code of v / div from its round-down code cf; saturates at 126.
+__device__ __forceinline__ int nearest_code(float v, float div, int cf, const Scale* tab) {
+    if (cf >= 126) return 126;
+    const float mid = 0.5f * div * (tab[cf].s + tab[cf + 1].s);   // exact
+    return (v > mid || (v == mid && ((cf + 1) & 1) == 0)) ? cf + 1 : cf;
+}
+
+// ---------------------------------------------------------------------------------------
+// Lane exchanges inside groups of 2 / 4 / 8 lanes (ds_swizzle, bit-mask mode: xor).
+// ---------------------------------------------------------------------------------------
+
+template <int XOR>
+__device__ __forceinline__ float swz_xor(float v) {
+    return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), (XOR << 10) | 0x1F));
+}
+
+template <int LPB>
+__device__ __forceinline__ float group_sum(float v) {
+    if (LPB >= 2) v += swz_xor<1>(v);
+    if (LPB >= 4) v += swz_xor<2>(v);
+    if (LPB >= 8) v += swz_xor<4>(v);
+    return v;
+}
+
+template <int LPB>
+__device__ __forceinline__ float group_max(float v) {
+    if (LPB >= 2) v = fmaxf(v, swz_xor<1>(v));
+    if (LPB >= 4) v = fmaxf(v, swz_xor<2>(v));
+    if (LPB >= 8) v = fmaxf(v, swz_xor<4>(v));
+    return v;
+}
+
+// ---------------------------------------------------------------------------------------
+// Loads.
+// ---------------------------------------------------------------------------------------
+
+template <typename In>
+struct Loader;
+
+template <>
+struct Loader<float> {
+    static __device__ __forceinline__ void load(const float* p, float (&v)[kLaneElems]) {
+        const float4* q = reinterpret_cast<const float4*>(p);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const float4 t = q[k];
+            v[4 * k] = t.x;
+            v[4 * k + 1] = t.y;
+            v[4 * k + 2] = t.z;
+            v[4 * k + 3] = t.w;
+        }
+    }
+};
+
+template <>
+struct Loader<uint16_t> {   // bfloat16 bit patterns; widening to binary32 is exact
+    static __device__ __forceinline__ void load(const uint16_t* p, float (&v)[kLaneElems]) {
+        const uint4* q = reinterpret_cast<const uint4*>(p);
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const uint4 t = q[k];
+            const uint32_t w[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                v[8 * k + 2 * j] = __uint_as_float(w[j] << 16);
+                v[8 * k + 2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+            }
+        }
+    }
+};
+
+__device__ __forceinline__ void load_weights(const float* p, float (&w)[kLaneElems]) {
+    const float4* q = reinterpret_cast<const float4*>(p);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const float4 t = q[k];
+        w[4 * k] = t.x;
+        w[4 * k + 1] = t.y;
+        w[4 * k + 2] = t.z;
+        w[4 * k + 3] = t.w;
+    }
+}
+
+// ---------------------------------------------------------------------------------------
+// Block loss of one candidate scale, binary32 (fast screen).
+// ---------------------------------------------------------------------------------------
+
+// u[i] ~ |y_i| / M (rounded once); the conversion divides by 2^E exactly and rounds to E2M1;
+// its decode gives g 2^E and e = |y| - (g 2^E) M is formed with one fused multiply-add.
+template <bool WEIGHTED>
+__device__ __forceinline__ float cand_loss(const float (&u)[kLaneElems], const float (&y)[kLaneElems],
+                                           const float (&w)[kLaneElems], float cvs, float M) {
+    float acc0 = 0.f, acc1 = 0.f;
+#pragma unroll
+    for (int i = 0; i < kLaneElems; i += 2) {
+        const uint32_t p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, u[i], u[i + 1], cvs, 0);
+        const float2v g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(p, cvs, 0);
+        const float e0 = fmaf(-g.x, M, fabsf(y[i]));
+        const float e1 = fmaf(-g.y, M, fabsf(y[i + 1]));
+        if (WEIGHTED) {
+            acc0 = fmaf(w[i] * e0, e0, acc0);
+            acc1 = fmaf(w[i + 1] * e1, e1, acc1);
+        } else {
+            acc0 = fmaf(e0, e0, acc0);
+            acc1 = fmaf(e1, e1, acc1);
+        }
+    }
+    return acc0 + acc1;
+}
+
+// Exactly rounded u = RN32(v / M) for M in [1, 2) with rM = RN32(1 / M) (Markstein).
+__device__ __forceinline__ float div_by_significand(float v, float M, float rM) {
+    const float u = v * rM;
+    const float r = fmaf(-u, M, v);
+    return fmaf(r, rM, u);
+}
+
+// Exact block loss in binary64, summed in element order 0..n-1 across the block's lanes:
+// e = |y| - g s exactly, term = e * e (times the weight), J = J + term.
+template <bool WEIGHTED, int LPB>
+__device__ double exact_loss(const float (&y)[kLaneElems], const float (&w)[kLaneElems], const Scale& sc,
+                             int part, int group_base_lane) {
+    double acc = 0.0;
+#pragma unroll 1
+    for (int l = 0; l < LPB; ++l) {
+        if (part == l) {
+#pragma unroll
+            for (int i = 0; i < kLaneElems; ++i) {
+                const float a = fabsf(y[i]);
+                const float u = div_by_significand(a, sc.M, sc.rM);
+                const uint32_t p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, u, 0.f, sc.cvs, 0);
+                const float2v g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(p, sc.cvs, 0);
+                const float gs = g.x * sc.M;                       // exact
+                const double e = (double)a - (double)gs;
+                double t = e * e;
+                if (WEIGHTED) t = (double)w[i] * t;
+                acc = acc + t;
+            }
+        }
+        if (LPB > 1) acc = __shfl(acc, group_base_lane + l, 64);
+    }
+    return acc;
+}
+
+// ---------------------------------------------------------------------------------------
+// Global scale: max |x| over the tensor.
+// ---------------------------------------------------------------------------------------
+
+__device__ __forceinline__ uint32_t absmax_bits(uint4 d, float) {
+    uint32_t m = d.x & 0x7FFFFFFFu;
+    m = max(m, d.y & 0x7FFFFFFFu);
+    m = max(m, d.z & 0x7FFFFFFFu);
+    return max(m, d.w & 0x7FFFFFFFu);
+}
+
+__device__ __forceinline__ uint32_t absmax_bits(uint4 d, uint16_t) {
+    // bfloat16 pairs: |x| bits of both halves, placed as binary32 bit patterns
+    uint32_t m = max((d.x << 16) & 0x7FFF0000u, d.x & 0x7FFF0000u);
+    m = max(m, max((d.y << 16) & 0x7FFF0000u, d.y & 0x7FFF0000u));
+    m = max(m, max((d.z << 16) & 0x7FFF0000u, d.z & 0x7FFF0000u));
+    return max(m, max((d.w << 16) & 0x7FFF0000u, d.w & 0x7FFF0000u));
+}
+
+// S = RN32(amax / denom) with denom = RN32(6 D); an all-zero tensor gets 1, an underflowing
+// quotient the smallest positive binary32, a non-finite input NaN.
+__device__ __forceinline__ float global_scale(uint32_t amax_bits, float denom) {
+    if (amax_bits >= 0x7F800000u) return __uint_as_float(0x7FC00000u);
+    if (amax_bits == 0u) return 1.0f;
+    const float s = __fdiv_rn(__uint_as_float(amax_bits), denom);
+    return s == 0.0f ? FLT_TRUE_MIN : s;
+}
+
+template <typename In>
+__global__ __launch_bounds__(kThreads) void amax_kernel(const In* __restrict__ x, int64_t nvec,
+                                                        float denom, uint32_t* __restrict__ ws,
+                                                        float* __restrict__ tensor_scale) {
+    const uint4* v = reinterpret_cast<const uint4*>(x);
+    uint32_t m = 0;
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    for (; i + 3 * stride < nvec; i += 4 * stride) {
+        const uint4 a = v[i], b = v[i + stride], c = v[i + 2 * stride], d = v[i + 3 * stride];
+        m = max(m, max(max(absmax_bits(a, In()), absmax_bits(b, In())),
+                       max(absmax_bits(c, In()), absmax_bits(d, In()))));
+    }
+    for (; i < nvec; i += stride) m = max(m, absmax_bits(v[i], In()));
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off, 64));
+    __shared__ uint32_t part[kThreads / 64];
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        m = max(max(part[0], part[1]), max(part[2], part[3]));
+        atomicMax(&ws[kWsAmax], m);
+        __threadfence();
+        const uint32_t arrived = atomicAdd(&ws[kWsCount], 1u);
+        if (arrived == gridDim.x - 1) {            // the last workgroup finalizes and resets
+            __threadfence();
+            const uint32_t bits = atomicAdd(&ws[kWsAmax], 0u);
+            const float S = global_scale(bits, denom);
+            const float rS = __fdiv_rn(1.0f, S);
+            tensor_scale[0] = S;
+            ws[kWsScale] = __float_as_uint(S);
+            ws[kWsRecip] = __float_as_uint(rS);
+            ws[kWsAmax] = 0u;
+            ws[kWsCount] = 0u;
+        }
+    }
+}
+
+__global__ void write_scale_kernel(float* tensor_scale, float S) { tensor_scale[0] = S; }
+
+// ---------------------------------------------------------------------------------------
+// Quantization kernel.
+// ---------------------------------------------------------------------------------------
+
+struct Params {
+    int64_t nblocks;          // micro-blocks in the tensor
+    uint32_t bpr;             // micro-blocks per row
+    uint32_t bpr_magic;       // blk / bpr = (umulhi(blk, magic) + ((blk - hi) >> 1)) >> (shift - 1)
+    uint32_t bpr_shift;
+    int dynamic;              // S, 1/S from the workspace (written by amax_kernel)
+    float S, rS;              // static global scale and its reciprocal
+    const uint32_t* ws;
+    float* tensor_scale;      // static path: written once
+};
+
+__device__ __forceinline__ uint32_t div_bpr(uint32_t n, const Params& p) {
+    if (p.bpr_shift == 0) return n;                       // bpr == 1
+    const uint32_t hi = __umulhi(n, p.bpr_magic);
+    return (hi + ((n - hi) >> 1)) >> (p.bpr_shift - 1);
+}
+
+template <int METHOD, int N>
+struct Window {
+    static constexpr int L = METHOD == kSweepMse
+                                 ? (N == 16 ? 3 : N == 32 ? 5 : N == 64 ? 7 : 11)
+                                 : (N == 128 ? 11 : 8);
+    static constexpr int U = 7;
+    static constexpr int NC = L + U + 1;
+};
+
+template <int METHOD, typename In, int N>
+__global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ x,
+                                                         const float* __restrict__ colw,
+                                                         uint8_t* __restrict__ q,
+                                                         uint8_t* __restrict__ scales, Params p) {
+    constexpr int LPB = N / kLaneElems;
+    constexpr bool WEIGHTED_OBJ = METHOD == kSweepWmse || METHOD == kFourSix;
+    __shared__ Scale tab[128];
+    fill_scale_table(tab);
+
+    const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t blk = gtid / LPB;
+    const int part = (int)(gtid % LPB);
+    const int lane = threadIdx.x & 63;
+    const int group_base = lane - part;
+    const bool active = blk < p.nblocks;
+    const int64_t blk_c = active ? blk : 0;   // inactive lanes run on block 0, store nothing
+
+    float S, rS;
+    if (p.dynamic) {
+        S = __uint_as_float(p.ws[kWsScale]);
+        rS = __uint_as_float(p.ws[kWsRecip]);
+    } else {
+        S = p.S;
+        rS = p.rS;
+        if (gtid == 0) p.tensor_scale[0] = S;
+    }
+    const bool fast_div = S >= 0x1p-26f && S <= 0x1p26f;
+
+    // ---- load and normalize y = RN32(x / S) -------------------------------------------
+    float y[kLaneElems];
+    Loader<In>::load(x + blk_c * N + part * kLaneElems, y);
+#pragma unroll
+    for (int i = 0; i < kLaneElems; ++i) {
+        const float xv = y[i];
+        if (fast_div && fabsf(xv) >= 0x1p-74f) {
+            y[i] = div_by_significand(xv, S, rS);    // exact for these ranges (Markstein)
+        } else {
+            y[i] = __fdiv_rn(xv, S);
+        }
+    }
+    float w[kLaneElems];
+    const bool use_w = WEIGHTED_OBJ && colw != nullptr;
+    if (use_w) {
+        const uint32_t row = div_bpr((uint32_t)blk_c, p);
+        const uint32_t kb = (uint32_t)blk_c - row * p.bpr;
+        load_weights(colw + (int64_t)kb * N + part * kLaneElems, w);
+    } else {
+#pragma unroll
+        for (int i = 0; i < kLaneElems; ++i) w[i] = 1.0f;
+    }
+
+    float ymax = 0.f;
+#pragma unroll
+    for (int i = 0; i < kLaneElems; ++i) ymax = fmaxf(ymax, fabsf(y[i]));
+    ymax = group_max<LPB>(ymax);
+
+    // ---- choose the block scale code ---------------------------------------------------
+    int code;
+    if (METHOD == kAbsMax) {
+        const int cf = floor_code(ymax, 6.0f, 1.0f / 6.0f, tab);
+        code = nearest_code(ymax, 6.0f, cf, tab);
+    } else if (METHOD == kFourSix) {
+        const int c6 = nearest_code(ymax, 6.0f, floor_code(ymax, 6.0f, 1.0f / 6.0f, tab), tab);
+        const int c4 = nearest_code(ymax, 4.0f, floor_code(ymax, 4.0f, 0.25f, tab), tab);
+        float u[kLaneElems];
+        const Scale s6 = tab[c6], s4 = tab[c4];
+#pragma unroll
+        for (int i = 0; i < kLaneElems; ++i) u[i] = fabsf(y[i]) * s6.rM;
+        float j6 = group_sum<LPB>(use_w ? cand_loss<true>(u, y, w, s6.cvs, s6.M)
+                                        : cand_loss<false>(u, y, w, s6.cvs, s6.M));
+#pragma unroll
+        for (int i = 0; i < kLaneElems; ++i) u[i] = fabsf(y[i]) * s4.rM;
+        float j4 = group_sum<LPB>(use_w ? cand_loss<true>(u, y, w, s4.cvs, s4.M)
+                                        : cand_loss<false>(u, y, w, s4.cvs, s4.M));
+        code = j4 < j6 ? c4 : c6;
+        const float lo = fminf(j4, j6), hi = fmaxf(j4, j6);
+        const bool near = c4 != c6 && !(hi > fmaf(lo, 2.0f * kBand, lo) + kBandAbs);
+        if (__any(near)) {
+            if (near) {
+                const double e6 = use_w ? exact_loss<true, LPB>(y, w, s6, part, group_base)
+                                        : exact_loss<false, LPB>(y, w, s6, part, group_base);
+                const double e4 = use_w ? exact_loss<true, LPB>(y, w, s4, part, group_base)
+                                        : exact_loss<false, LPB>(y, w, s4, part, group_base);
+                code = e4 < e6 ? c4 : c6;
+            }
+        }
+    } else {
+        using Win = Window<METHOD, N>;
+        constexpr int NC = Win::NC;
+        constexpr bool WGT = METHOD == kSweepWmse;
+        const int c0 = floor_code(ymax, 6.0f, 1.0f / 6.0f, tab);
+        const int cb = c0 - Win::L;                 // candidate d is code cb + d
+        float J[NC];
+        if (__all(cb >= 8)) {
+            // normal codes only: c, c+8, c+16 share the significand M and differ in 2^E
+#pragma unroll
+            for (int d = 0; d < 8 && d < NC; ++d) {
+                const Scale s0 = tab[clamp_code(cb + d)];
+                float u[kLaneElems];
+#pragma unroll
+                for (int i = 0; i < kLaneElems; ++i) u[i] = fabsf(y[i]) * s0.rM;
+#pragma unroll
+                for (int j = d; j < NC; j += 8) {
+                    const Scale sj = tab[clamp_code(cb + j)];
+                    J[j] = group_sum<LPB>(cand_loss<WGT>(u, y, w, sj.cvs, sj.M));
+                }
+            }
+        } else {
+#pragma unroll
+            for (int d = 0; d < NC; ++d) {
+                const Scale sd = tab[clamp_code(cb + d)];
+                float u[kLaneElems];
+#pragma unroll
+                for (int i = 0; i < kLaneElems; ++i) u[i] = fabsf(y[i]) * sd.rM;
+                J[d] = group_sum<LPB>(cand_loss<WGT>(u, y, w, sd.cvs, sd.M));
+            }
+        }
+        // codes outside 1..126 are not candidates
+#pragma unroll
+        for (int d = 0; d < NC; ++d)
+            if (cb + d < 1 || cb + d > 126) J[d] = __uint_as_float(0x7F800000u);
+        // argmin on the loss with its 7 low bits replaced by the candidate index: exact
+        // ordering except between losses within 2^-16 of each other, which the band re-scores
+        uint32_t best = 0xFFFFFFFFu;
+#pragma unroll
+        for (int d = 0; d < NC; ++d) best = min(best, (__float_as_uint(J[d]) & 0xFFFFFF80u) | (uint32_t)d);
+        int dstar = (int)(best & 0x7Fu);
+        const float j1 = __uint_as_float(best & 0xFFFFFF80u);
+        const float bound = fmaf(j1, kBand, j1) + kBandAbs;
+        uint64_t seen1 = 0, seen2 = 0;
+#pragma unroll
+        for (int d = 0; d < NC; ++d) {
+            const uint64_t m = __ballot(J[d] <= bound);
+            seen2 |= seen1 & m;
+            seen1 |= m;
+        }
+        const bool near = (seen2 >> lane) & 1ull;
+        if (seen2 != 0ull) {
+            if (near) {
+                double jb = 0.0;
+                int db = -1;
+#pragma unroll 1
+                for (int d = 0; d < NC; ++d) {
+                    if (J[d] <= bound && cb + d >= 1 && cb + d <= 126) {
+                        const Scale sd = tab[clamp_code(cb + d)];
+                        const double jd = exact_loss<WGT, LPB>(y, w, sd, part, group_base);
+                        if (db < 0 || jd < jb) {
+                            jb = jd;
+                            db = d;
+                        }
+                    }
+                }
+                if (db >= 0) dstar = db;
+            }
+        }
+        code = clamp_code(cb + dstar);   // always a window code unless every loss is NaN
+    }
+
+    // ---- emit: exact FP4 codes at the chosen scale, packed two per byte ------------------
+    const Scale sc = tab[code];
+    uint32_t packed[2] = {0u, 0u};
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        float u[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const float v = y[8 * h + i];
+            const float t = div_by_significand(v, sc.M, sc.rM);
+            u[i] = __uint_as_float((__float_as_uint(t) & 0x7FFFFFFFu) | (__float_as_uint(v) & 0x80000000u));
+        }
+        uint32_t r = 0u;
+        r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, u[0], u[1], sc.cvs, 0);
+        r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, u[2], u[3], sc.cvs, 1);
+        r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, u[4], u[5], sc.cvs, 2);
+        r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, u[6], u[7], sc.cvs, 3);
+        packed[h] = r;
+    }
+    if (active) {
+        uint2* dst = reinterpret_cast<uint2*>(q + ((blk * N + part * kLaneElems) >> 1));
+        *dst = make_uint2(packed[0], packed[1]);
+        if (part == 0) scales[blk] = (uint8_t)code;
+    }
+}
+
+// ---------------------------------------------------------------------------------------
+// Dequantization: x_hat = RN32((q s) S), 16 elements per lane.
+// ---------------------------------------------------------------------------------------
+
+template <int N>
+__global__ __launch_bounds__(kThreads) void dequant_kernel(const uint8_t* __restrict__ q,
+                                                           const uint8_t* __restrict__ scales,
+                                                           const float* __restrict__ tensor_scale,
+                                                           int64_t nseg, float* __restrict__ out) {
+    const int64_t seg = (int64_t)blockIdx.x * kThreads + threadIdx.x;    // 16-element segment
+    if (seg >= nseg) return;
+    const float S = tensor_scale[0];
+    const uint2 pk = reinterpret_cast<const uint2*>(q)[seg];
+    const int code = scales[(seg * kLaneElems) / N];
+    const float s = e4m3_value(code);
+    const float cvs = code == 0 ? 1.0f : s;
+    const float M = code == 0 ? 0.f : __uint_as_float((__float_as_uint(s) & 0x007FFFFFu) | 0x3F800000u);
+    const uint32_t words[2] = {pk.x, pk.y};
+    float o[kLaneElems];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            float2v g;
+            switch (b) {   // the byte selector must be a constant
+                case 0: g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(words[h], cvs, 0); break;
+                case 1: g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(words[h], cvs, 1); break;
+                case 2: g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(words[h], cvs, 2); break;
+                default: g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(words[h], cvs, 3); break;
+            }
+            o[8 * h + 2 * b] = (g.x * M) * S;        // g 2^E M = q s exactly, then one rounding
+            o[8 * h + 2 * b + 1] = (g.y * M) * S;
+        }
+    }
+    float4* dst = reinterpret_cast<float4*>(out + seg * kLaneElems);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) dst[k] = make_float4(o[4 * k], o[4 * k + 1], o[4 * k + 2], o[4 * k + 3]);
+}
+
+// ---------------------------------------------------------------------------------------
+// Host side.
+// ---------------------------------------------------------------------------------------
+
+bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+bool valid_block(int block) { return block == 16 || block == 32 || block == 64 || block == 128; }
+
+// Unsigned division by an invariant d >= 1: magic m and shift l with
+// n / d = (hi + ((n - hi) >> 1)) >> (l - 1), hi = umulhi(n, m), l = ceil(log2 d) (l = 0: d = 1).
+void make_divider(uint32_t d, uint32_t* magic, uint32_t* shift) {
+    uint32_t l = 0;
+    while ((1ull << l) < d) ++l;
+    *shift = l;
+    *magic = l == 0 ? 0u : (uint32_t)((((1ull << l) - d) << 32) / d + 1);
+}
+
+struct Call {
+    int method;
+    const void* x;
+    int dtype;
+    int64_t rows, cols;
+    int block;
+    const float* colw;
+    float fp8_range, static_scale;
+    float* tensor_scale;
+    uint8_t* q;
+    uint8_t* scales;
+    void* ws;
+    size_t ws_bytes;
+    hipStream_t stream;
+};
+
+template <int METHOD, typename In, int N>
+hipError_t launch_quant(const Call& c, const Params& p) {
+    constexpr int LPB = N / kLaneElems;
+    const int64_t lanes = p.nblocks * LPB;
+    const int64_t grid = (lanes + kThreads - 1) / kThreads;
+    hipLaunchKernelGGL((quant_kernel<METHOD, In, N>), dim3((unsigned)grid), dim3(kThreads), 0, c.stream,
+                       static_cast<const In*>(c.x), c.colw, c.q, c.scales, p);
+    return hipGetLastError();
+}
+
+template <int METHOD, typename In>
+hipError_t launch_quant_n(const Call& c, const Params& p) {
+    switch (c.block) {
+        case 16: return launch_quant<METHOD, In, 16>(c, p);
+        case 32: return launch_quant<METHOD, In, 32>(c, p);
+        case 64: return launch_quant<METHOD, In, 64>(c, p);
+        default: return launch_quant<METHOD, In, 128>(c, p);
+    }
+}
+
+template <int METHOD>
+hipError_t launch_quant_m(const Call& c, const Params& p) {
+    return c.dtype == NVFP4_IN_F32 ? launch_quant_n<METHOD, float>(c, p)
+                                   : launch_quant_n<METHOD, uint16_t>(c, p);
+}
+
+int run_quant(const Call& c) {
+    if (!c.tensor_scale) return NVFP4_ERR_NULL;
+    if (c.dtype != NVFP4_IN_F32 && c.dtype != NVFP4_IN_BF16) return NVFP4_ERR_DTYPE;
+    if (!valid_block(c.block)) return NVFP4_ERR_BLOCK;
+    if (c.rows < 0 || c.cols < 0 || c.cols % c.block != 0) return NVFP4_ERR_SHAPE;
+    if (!(c.fp8_range > 0.0f && c.fp8_range <= 448.0f)) return NVFP4_ERR_ARG;
+    if (!(c.static_scale >= 0.0f && c.static_scale <= FLT_MAX)) return NVFP4_ERR_ARG;
+    if (c.method == kSweepWmse && !c.colw) return NVFP4_ERR_NULL;
+    const int64_t n = c.rows * c.cols;
+    if (n > 0 && (!c.x || !c.q || !c.scales)) return NVFP4_ERR_NULL;
+    const bool dynamic = c.static_scale == 0.0f;
+    if (dynamic) {
+        if (!c.ws) return NVFP4_ERR_WORKSPACE;
+        if (c.ws_bytes < kWorkspaceBytes) return NVFP4_ERR_WORKSPACE;
+        if (!aligned(c.ws, 16)) return NVFP4_ERR_ALIGN;
+    }
+    if (n > 0 && (!aligned(c.x, 16) || !aligned(c.q, 8))) return NVFP4_ERR_ALIGN;
+    if (c.colw && !aligned(c.colw, 16)) return NVFP4_ERR_ALIGN;
+    const int64_t nblocks = n / c.block;
+    if (nblocks > 0x7FFFFFFFLL) return NVFP4_ERR_SHAPE;     // 32-bit block indexing
+
+    hipError_t err = hipSuccess;
+    const float denom = 6.0f * c.fp8_range;
+    if (dynamic) {
+        const int64_t nvec = n * (c.dtype == NVFP4_IN_F32 ? 4 : 2) / 16;
+        int64_t g = (nvec + kThreads * 4 - 1) / (kThreads * 4);
+        if (g < 1) g = 1;
+        if (g > 2048) g = 2048;
+        if (c.dtype == NVFP4_IN_F32)
+            hipLaunchKernelGGL(amax_kernel<float>, dim3((unsigned)g), dim3(kThreads), 0, c.stream,
+                               static_cast<const float*>(c.x), nvec, denom,
+                               static_cast<uint32_t*>(c.ws), c.tensor_scale);
+        else
+            hipLaunchKernelGGL(amax_kernel<uint16_t>, dim3((unsigned)g), dim3(kThreads), 0, c.stream,
+                               static_cast<const uint16_t*>(c.x), nvec, denom,
+                               static_cast<uint32_t*>(c.ws), c.tensor_scale);
+        err = hipGetLastError();
+    } else if (nblocks == 0) {
+        hipLaunchKernelGGL(write_scale_kernel, dim3(1), dim3(1), 0, c.stream, c.tensor_scale,
+                           c.static_scale);
+        err = hipGetLastError();
+    }
+    if (err != hipSuccess) return NVFP4_ERR_HIP;
+    if (nblocks == 0) return NVFP4_OK;
+
+    Params p;
+    p.nblocks = nblocks;
+    p.bpr = (uint32_t)(c.cols / c.block);
+    make_divider(p.bpr, &p.bpr_magic, &p.bpr_shift);
+    p.dynamic = dynamic ? 1 : 0;
+    p.S = dynamic ? 0.0f : c.static_scale;
+    p.rS = dynamic ? 0.0f : 1.0f / c.static_scale;
+    p.ws = static_cast<const uint32_t*>(c.ws);
+    p.tensor_scale = c.tensor_scale;
+    switch (c.method) {
+        case kAbsMax: err = launch_quant_m<kAbsMax>(c, p); break;
+        case kFourSix: err = launch_quant_m<kFourSix>(c, p); break;
+        case kSweepMse: err = launch_quant_m<kSweepMse>(c, p); break;
+        default: err = launch_quant_m<kSweepWmse>(c, p); break;
+    }
+    return err == hipSuccess ? NVFP4_OK : NVFP4_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t nvfp4_workspace_bytes(void) { return kWorkspaceBytes; }
+
+const char* nvfp4_status_string(int status) {
+    switch (status) {
+        case NVFP4_OK: return "ok";
+        case NVFP4_ERR_NULL: return "a required pointer is NULL";
+        case NVFP4_ERR_SHAPE: return "bad shape (rows/cols negative, cols not a multiple of block, or too many blocks)";
+        case NVFP4_ERR_BLOCK: return "block must be 16, 32, 64 or 128";
+        case NVFP4_ERR_DTYPE: return "unsupported dtype";
+        case NVFP4_ERR_ARG: return "fp8_range or static_scale out of range";
+        case NVFP4_ERR_WORKSPACE: return "dynamic global scale needs a workspace of nvfp4_workspace_bytes() bytes";
+        case NVFP4_ERR_ALIGN: return "misaligned pointer (x, col_weight, workspace: 16 bytes; q: 8 bytes)";
+        case NVFP4_ERR_HIP: return "HIP kernel launch failed";
+        default: return "unknown status";
+    }
+}
+
+int nvfp4_quant_absmax(const void* x, int dtype, int64_t rows, int64_t cols, int block,
+                       float fp8_range, float static_scale, float* tensor_scale, uint8_t* q,
+                       uint8_t* scales, void* workspace, size_t workspace_bytes, void* stream) {
+    return run_quant({kAbsMax, x, dtype, rows, cols, block, nullptr, fp8_range, static_scale,
+                      tensor_scale, q, scales, workspace, workspace_bytes, (hipStream_t)stream});
+}
+
+int nvfp4_quant_four_over_six(const void* x, int dtype, int64_t rows, int64_t cols, int block,
+                              const float* col_weight, float fp8_range, float static_scale,
+                              float* tensor_scale, uint8_t* q, uint8_t* scales,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+    return run_quant({kFourSix, x, dtype, rows, cols, block, col_weight, fp8_range, static_scale,
+                      tensor_scale, q, scales, workspace, workspace_bytes, (hipStream_t)stream});
+}
+
+int nvfp4_quant_scalesweep_mse(const void* x, int dtype, int64_t rows, int64_t cols, int block,
+                               float fp8_range, float static_scale, float* tensor_scale,
+                               uint8_t* q, uint8_t* scales, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+    return run_quant({kSweepMse, x, dtype, rows, cols, block, nullptr, fp8_range, static_scale,
+                      tensor_scale, q, scales, workspace, workspace_bytes, (hipStream_t)stream});
+}
+
+int nvfp4_quant_scalesweep_wmse(const void* x, int dtype, int64_t rows, int64_t cols, int block,
+                                const float* col_weight, float fp8_range, float static_scale,
+                                float* tensor_scale, uint8_t* q, uint8_t* scales,
+                                void* workspace, size_t workspace_bytes, void* stream) {
+    return run_quant({kSweepWmse, x, dtype, rows, cols, block, col_weight, fp8_range,
+                      static_scale, tensor_scale, q, scales, workspace, workspace_bytes,
+                      (hipStream_t)stream});
+}
+
+int nvfp4_dequant(const uint8_t* q, const uint8_t* scales, const float* tensor_scale,
+                  int64_t rows, int64_t cols, int block, int out_dtype, void* out, void* stream) {
+    if (!tensor_scale) return NVFP4_ERR_NULL;
+    if (out_dtype != NVFP4_IN_F32) return NVFP4_ERR_DTYPE;
+    if (!valid_block(block)) return NVFP4_ERR_BLOCK;
+    if (rows < 0 || cols < 0 || cols % block != 0) return NVFP4_ERR_SHAPE;
+    const int64_t n = rows * cols;
+    if (n == 0) return NVFP4_OK;
+    if (!q || !scales || !out) return NVFP4_ERR_NULL;
+    if (!aligned(q, 8) || !aligned(out, 16)) return NVFP4_ERR_ALIGN;
+    const int64_t nseg = n / kLaneElems;
+    const int64_t grid = (nseg + kThreads - 1) / kThreads;
+    hipStream_t s = (hipStream_t)stream;
+    switch (block) {
+        case 16: hipLaunchKernelGGL(dequant_kernel<16>, dim3((unsigned)grid), dim3(kThreads), 0, s, q, scales, tensor_scale, nseg, (float*)out); break;
+        case 32: hipLaunchKernelGGL(dequant_kernel<32>, dim3((unsigned)grid), dim3(kThreads), 0, s, q, scales, tensor_scale, nseg, (float*)out); break;
+        case 64: hipLaunchKernelGGL(dequant_kernel<64>, dim3((unsigned)grid), dim3(kThreads), 0, s, q, scales, tensor_scale, nseg, (float*)out); break;
+        default: hipLaunchKernelGGL(dequant_kernel<128>, dim3((unsigned)grid), dim3(kThreads), 0, s, q, scales, tensor_scale, nseg, (float*)out); break;
+    }
+    return hipGetLastError() == hipSuccess ? NVFP4_OK : NVFP4_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,141 @@
+"""ctypes binding of libnvfp4ss.so: the C entry points under their own names, plus
+``quantize`` / ``dequant`` helpers that allocate outputs with torch on the input's device and
+pass raw device pointers and the current HIP stream."""
+from __future__ import annotations
+
+import ctypes
+from pathlib import Path
+
+import torch
+
+LIB_PATH = Path(__file__).resolve().parent / "libnvfp4ss.so"
+
+F32, BF16 = 0, 1
+STATUS = {
+    0: "ok", -1: "null pointer", -2: "bad shape", -3: "bad block", -4: "bad dtype",
+    -5: "bad argument", -6: "workspace", -7: "alignment", -8: "HIP launch failed",
+}
+DEFAULT_RANGE = {"absmax": 448.0, "four_over_six": 256.0, "scalesweep_mse": 256.0,
+                 "scalesweep_wmse": 256.0}
+
+
+class NVFP4Error(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: status {status} ({STATUS.get(status, '?')})")
+        self.status = status
+
+
+def _load():
+    if not LIB_PATH.exists():
+        raise ImportError(f"{LIB_PATH} is not built; run `python -c 'import __graft_entry__ as g; "
+                          "g.build()'` (hipcc for gfx950)")
+    L = ctypes.CDLL(str(LIB_PATH))
+    P, I64, I, F, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    quant = [P, I, I64, I64, I, F, F, P, P, P, P, SZ, P]
+    quant_w = [P, I, I64, I64, I, P, F, F, P, P, P, P, SZ, P]
+    sigs = {
+        "nvfp4_workspace_bytes": (SZ, []),
+        "nvfp4_status_string": (ctypes.c_char_p, [I]),
+        "nvfp4_quant_absmax": (I, quant),
+        "nvfp4_quant_four_over_six": (I, quant_w),
+        "nvfp4_quant_scalesweep_mse": (I, quant),
+        "nvfp4_quant_scalesweep_wmse": (I, quant_w),
+        "nvfp4_dequant": (I, [P, P, P, I64, I64, I, I, P, P]),
+    }
+    for name, (res, args) in sigs.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    return L
+
+
+lib = _load()
+
+# The C entry points, under the header's names.
+nvfp4_workspace_bytes = lib.nvfp4_workspace_bytes
+nvfp4_status_string = lib.nvfp4_status_string
+nvfp4_quant_absmax = lib.nvfp4_quant_absmax
+nvfp4_quant_four_over_six = lib.nvfp4_quant_four_over_six
+nvfp4_quant_scalesweep_mse = lib.nvfp4_quant_scalesweep_mse
+nvfp4_quant_scalesweep_wmse = lib.nvfp4_quant_scalesweep_wmse
+nvfp4_dequant = lib.nvfp4_dequant
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def workspace(device) -> torch.Tensor:
+    """A zero-filled workspace for the dynamic-scale path (reusable by sequential calls on
+    one stream; every call leaves it zero-filled again)."""
+    return torch.zeros(nvfp4_workspace_bytes() // 4, dtype=torch.int32, device=device)
+
+
+def quantize(x: torch.Tensor, method: str = "scalesweep_wmse", block: int = 16,
+             weight: torch.Tensor | None = None, fp8_range: float | None = None,
+             static_scale: float = 0.0, ws: torch.Tensor | None = None, out=None):
+    """Quantize a 2-D device tensor [rows, cols] (bfloat16 or float32) to NVFP4.
+
+    Returns (q [rows, cols/2] uint8, scales [rows, cols/block] uint8, S [1] float32), all on
+    x's device; the work is enqueued on the current stream.  ``out`` may pass preallocated
+    (q, scales, S) tensors."""
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D [rows, cols]")
+    if not x.is_cuda:
+        raise ValueError("x must be a device tensor (the library runs on the GPU only)")
+    if not x.is_contiguous():
+        raise ValueError("x must be contiguous")
+    if x.dtype == torch.bfloat16:
+        dt = BF16
+    elif x.dtype == torch.float32:
+        dt = F32
+    else:
+        raise TypeError("x must be bfloat16 or float32")
+    rows, cols = x.shape
+    D = DEFAULT_RANGE[method] if fp8_range is None else float(fp8_range)
+    if out is None:
+        q = torch.empty((rows, cols // 2), dtype=torch.uint8, device=x.device)
+        sc = torch.empty((rows, cols // block if block else 0), dtype=torch.uint8, device=x.device)
+        S = torch.empty(1, dtype=torch.float32, device=x.device)
+    else:
+        q, sc, S = out
+    if static_scale == 0.0 and ws is None:
+        ws = workspace(x.device)
+    wsb = 0 if ws is None else ws.numel() * ws.element_size()
+    common = (_ptr(x), dt, rows, cols, block)
+    tail = (ctypes.c_float(D), ctypes.c_float(static_scale), _ptr(S), _ptr(q), _ptr(sc),
+            _ptr(ws), wsb, _stream(x.device))
+    if weight is not None:
+        if not (weight.is_cuda and weight.dtype == torch.float32 and weight.is_contiguous()
+                and weight.numel() == cols):
+            raise ValueError("weight must be a contiguous float32 device tensor of length cols")
+    if method == "absmax":
+        rc = nvfp4_quant_absmax(*common, *tail)
+    elif method == "four_over_six":
+        rc = nvfp4_quant_four_over_six(*common, _ptr(weight), *tail)
+    elif method == "scalesweep_mse":
+        rc = nvfp4_quant_scalesweep_mse(*common, *tail)
+    elif method == "scalesweep_wmse":
+        rc = nvfp4_quant_scalesweep_wmse(*common, _ptr(weight), *tail)
+    else:
+        raise ValueError(f"unknown method {method!r}")
+    if rc != 0:
+        raise NVFP4Error(rc, f"nvfp4_quant_{method}")
+    return q, sc, S
+
+
+def dequant(q: torch.Tensor, scales: torch.Tensor, S: torch.Tensor, block: int = 16,
+            out: torch.Tensor | None = None) -> torch.Tensor:
+    """x_hat [rows, cols] float32 from (q, scales, S)."""
+    rows, cols = q.shape[0], q.shape[1] * 2
+    if out is None:
+        out = torch.empty((rows, cols), dtype=torch.float32, device=q.device)
+    rc = nvfp4_dequant(_ptr(q), _ptr(scales), _ptr(S), rows, cols, block, F32, _ptr(out),
+                       _stream(q.device))
+    if rc != 0:
+        raise NVFP4Error(rc, "nvfp4_dequant")
+    return out

@@ -1,0 +1,256 @@
+"""GPU parity: the HIP path (through the C interface) against the CPU oracle, bit for bit.
+
+Codes, scale bytes, nibbles and the global scale must be identical: the kernels re-decide
+near-ties in binary64 exactly as the oracle sums them, so no block is exempt.  Inputs are
+seeded and synthetic (workloads.py); the oracle receives the same bytes, copied to the host.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+METHODS = ["absmax", "four_over_six", "scalesweep_mse", "scalesweep_wmse"]
+RANGE = {"absmax": 448.0, "four_over_six": 256.0, "scalesweep_mse": 256.0,
+         "scalesweep_wmse": 256.0}
+
+
+@pytest.fixture(scope="module")
+def nv():
+    assert torch.cuda.is_available(), "GPU parity tests need a GPU"
+    import paper_2606_07618_amd as nv
+    return nv
+
+
+DEV = "cuda:0"
+
+
+def describe_mismatch(a, b, what):
+    bad = np.argwhere(a != b)
+    return f"{what}: {len(bad)} mismatches, first at {bad[:5].tolist()}: gpu {a[tuple(bad[0])]} oracle {b[tuple(bad[0])]}"
+
+
+def check(nv, method, x, block=16, w=None, static=0.0, D=None, rows_sample=None):
+    """Quantize on the GPU, then compare with the oracle (optionally on a subset of rows,
+    with the oracle's own global scale of the whole tensor)."""
+    D = RANGE[method] if D is None else D
+    use_w = w if method in ("scalesweep_wmse", "four_over_six") else None
+    q, sc, S = nv.quantize(x, method, block, weight=use_w, fp8_range=D, static_scale=static)
+    torch.cuda.synchronize()
+    xh = workloads.host_array(x)
+    wh = None if use_w is None else use_w.cpu().numpy()
+    if rows_sample is None:
+        S_ref, q_ref, sc_ref = oracle.quantize(method, xh, block, D, static, wh)
+        qg, scg = q.cpu().numpy(), sc.cpu().numpy()
+    else:
+        S_ref = static if static else oracle.tensor_scale(xh, D)
+        _, q_ref, sc_ref = oracle.quantize(method, xh[rows_sample], block, D, S_ref, wh)
+        qg, scg = q[rows_sample].cpu().numpy(), sc[rows_sample].cpu().numpy()
+    S_gpu = S.cpu().numpy()[0]
+    assert np.float32(S_gpu).view(np.uint32) == np.float32(S_ref).view(np.uint32), (S_gpu, S_ref)
+    assert np.array_equal(scg, sc_ref), describe_mismatch(scg, sc_ref, "scales")
+    assert np.array_equal(qg, q_ref), describe_mismatch(qg, q_ref, "nibbles")
+    return q, sc, S
+
+
+# ---------------------------------------------------------------------------------------
+# Small shapes: several workgroups with a ragged tail, every method / dtype / block size.
+# ---------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("method", METHODS)
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("block", [16, 32, 64, 128])
+@pytest.mark.parametrize("static", [0.0, 3.0e-4])
+def test_parity_small(nv, method, dtype, block, static):
+    g = workloads.generator(DEV, 1, block, 0 if dtype == torch.bfloat16 else 1)
+    rows, cols = 131, 4 * 128
+    x = workloads.llm_weight(rows, cols, g, DEV, outlier_frac=0.01).to(dtype)
+    w = workloads.column_importance(cols, g, DEV, tokens=128)
+    check(nv, method, x, block, w, static)
+
+
+@pytest.mark.parametrize("method", METHODS)
+def test_parity_c0_matrix(nv, method):
+    """binary32 [1024, 1024] N(0, 1) from default_rng(0), block 16, S = amax / (6 * 448)."""
+    x = torch.from_numpy(workloads.c0_matrix()).to(DEV)
+    w = workloads.column_importance(1024, workloads.generator(DEV, 0, 7), DEV, tokens=256)
+    check(nv, method, x, 16, w, D=448.0)
+
+
+# ---------------------------------------------------------------------------------------
+# Edge cases.
+# ---------------------------------------------------------------------------------------
+
+def _edge_tensors():
+    rng = np.random.default_rng(5)
+    out = {}
+    out["zeros"] = np.zeros((4, 64), np.float32)
+    z = np.zeros((4, 64), np.float32)
+    z[2, 17] = -3.5
+    out["single_nonzero"] = z
+    nz = np.zeros((3, 64), np.float32)
+    nz[0, ::2] = -0.0
+    nz[1, 5] = 1.0
+    out["negative_zeros"] = nz
+    out["constant"] = np.full((5, 64), 0.37, np.float32)
+    # elements exactly on FP4 midpoints of the AbsMax scale (S = 1 static below)
+    mids = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0, 6.0], np.float32)
+    m = np.tile(np.concatenate([mids, -mids]), (8, 4)).astype(np.float32)
+    m[:, 0] = 6.0
+    out["midpoints"] = m
+    # blocks far below the tensor max: subnormal E4M3 scale codes
+    t = (rng.standard_normal((8, 128)) * 1e-4).astype(np.float32)
+    t[0, 0] = 50.0
+    out["subnormal_s0"] = t
+    # inputs below 2^-74 next to normal ones (IEEE-division fallback of the normalization)
+    u = (rng.standard_normal((4, 64))).astype(np.float32)
+    u[:, 1::7] *= np.float32(1e-30)
+    u[1, 3] = np.float32(1e-40)
+    out["tiny_values"] = u
+    # tiny tensor maximum: subnormal global scale
+    v = (rng.standard_normal((4, 64)) * 1e-37).astype(np.float32)
+    out["tiny_amax"] = v
+    # one outlier column x1000
+    o = rng.standard_normal((16, 256)).astype(np.float32)
+    o[:, 77] *= 1000
+    out["outlier_column"] = o
+    return out
+
+
+EDGES = _edge_tensors()
+
+
+@pytest.mark.parametrize("name", list(EDGES))
+@pytest.mark.parametrize("method", METHODS)
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_parity_edges(nv, name, method, dtype):
+    x = torch.from_numpy(EDGES[name]).to(DEV).to(dtype)
+    w = torch.linspace(0.1, 3.0, x.shape[1], device=DEV)
+    check(nv, method, x, 16, w)
+    if name == "midpoints":
+        check(nv, method, x, 16, w, static=1.0)
+
+
+@pytest.mark.parametrize("method", METHODS)
+def test_parity_saturating_static_scale(nv, method):
+    """A static S far too small: block maxima beyond 6 * 448 saturate the scale code at 126
+    and the nibbles at 6."""
+    g = workloads.generator(DEV, 3, 3)
+    x = workloads.llm_weight(32, 256, g, DEV)
+    w = workloads.column_importance(256, g, DEV, tokens=64)
+    check(nv, method, x, 16, w, static=1e-7)
+
+
+def test_all_bfloat16_patterns(nv):
+    """Every finite bfloat16 value (as a [4094, 16] tensor, sign-interleaved) under several
+    static global scales: exercises the exact normalization on the whole input format."""
+    all_bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    f = (all_bits.astype(np.uint32) << 16).view(np.float32)
+    w = torch.linspace(0.5, 2.0, 16, device=DEV)
+    for S in (1.0, 3.0e-3, 7.1e2, 1.0e30):
+        # keep the patterns whose quotient x / S is finite (a static S must allow that)
+        with np.errstate(invalid="ignore"):
+            keep = np.isfinite(f) & (np.abs(f.astype(np.float64)) / S < 3.0e38)
+        bits = all_bits[keep]
+        n = (bits.size // 16) * 16
+        xb = torch.from_numpy(bits[:n].view(np.int16).reshape(-1, 16)).to(DEV).view(torch.bfloat16)
+        for method in ("absmax", "scalesweep_mse", "scalesweep_wmse"):
+            check(nv, method, xb, 16, w, static=S)
+
+
+def test_nonfinite_input_gives_nan_scale(nv):
+    x = torch.randn(8, 64, device=DEV)
+    x[3, 9] = float("nan")
+    q, sc, S = nv.quantize(x, "scalesweep_mse", 16)
+    torch.cuda.synchronize()
+    assert torch.isnan(S).item()
+    x[3, 9] = float("inf")
+    q, sc, S = nv.quantize(x, "absmax", 16)
+    torch.cuda.synchronize()
+    assert torch.isnan(S).item()
+
+
+def test_empty_tensor(nv):
+    x = torch.zeros(0, 64, device=DEV, dtype=torch.bfloat16)
+    q, sc, S = nv.quantize(x, "scalesweep_mse", 16)
+    torch.cuda.synchronize()
+    assert S.item() == 1.0 and q.numel() == 0
+    q, sc, S = nv.quantize(x, "scalesweep_mse", 16, static_scale=0.5)
+    torch.cuda.synchronize()
+    assert S.item() == 0.5
+
+
+def test_workspace_left_zero_and_reusable(nv):
+    ws = nv.workspace(DEV)
+    g = workloads.generator(DEV, 4, 4)
+    for i in range(3):
+        x = workloads.llm_weight(64 + 64 * i, 512, g, DEV)
+        check_q = nv.quantize(x, "scalesweep_mse", 16, ws=ws)
+        torch.cuda.synchronize()
+        assert int(ws[0].item()) == 0 and int(ws[1].item()) == 0
+        S_ref = oracle.tensor_scale(workloads.host_array(x), 256.0)
+        assert check_q[2].item() == S_ref
+
+
+def test_deterministic_and_stream_ordered(nv):
+    g = workloads.generator(DEV, 5, 5)
+    x = workloads.llm_weight(512, 1024, g, DEV)
+    w = workloads.column_importance(1024, g, DEV, tokens=64)
+    r1 = nv.quantize(x, "scalesweep_wmse", 16, weight=w)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        r2 = nv.quantize(x, "scalesweep_wmse", 16, weight=w)
+    torch.cuda.synchronize()
+    for a, b in zip(r1, r2):
+        assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("block", [16, 32, 64, 128])
+@pytest.mark.parametrize("method", ["absmax", "scalesweep_wmse"])
+def test_dequant_parity(nv, block, method):
+    g = workloads.generator(DEV, 6, block)
+    x = workloads.llm_weight(96, 512, g, DEV)
+    w = workloads.column_importance(512, g, DEV, tokens=64)
+    q, sc, S = check(nv, method, x, block, w)
+    xh = nv.dequant(q, sc, S, block)
+    torch.cuda.synchronize()
+    ref = oracle.dequant(q.cpu().numpy(), sc.cpu().numpy(), S.item(), block)
+    assert np.array_equal(xh.cpu().numpy().view(np.uint32), ref.view(np.uint32))
+
+
+# ---------------------------------------------------------------------------------------
+# Full-size workloads, in the launch configuration the benchmark times: sampled rows,
+# against the oracle's global scale of the whole tensor.
+# ---------------------------------------------------------------------------------------
+
+def _sample_rows(rows, k, seed):
+    return np.sort(np.random.default_rng(seed).choice(rows, size=min(k, rows), replace=False))
+
+
+@pytest.mark.parametrize("method", METHODS)
+def test_parity_llama8b_layer_sampled(nv, method):
+    layer = workloads.llama8b_layer(DEV)
+    for i, (name, (x, w)) in enumerate(layer.items()):
+        rows = _sample_rows(x.shape[0], 48, i)
+        check(nv, method, x, 16, w, rows_sample=rows)
+
+
+@pytest.mark.parametrize("block", [16, 32, 64, 128])
+def test_parity_square8192_sampled(nv, block):
+    x, w = workloads.square8192(DEV)
+    rows = _sample_rows(8192, 24, block)
+    for method in METHODS:
+        check(nv, method, x, block, w, rows_sample=rows)
+
+
+def test_parity_online_sampled(nv):
+    t = workloads.online_tensors(DEV)
+    for i, (name, v) in enumerate(t.items()):
+        x = v.reshape(-1, v.shape[-1])
+        rows = _sample_rows(x.shape[0], 256, 100 + i)
+        check(nv, "scalesweep_mse", x, 16, rows_sample=rows)
+        check(nv, "scalesweep_mse", x, 16, static=0.01, rows_sample=rows)
+        check(nv, "absmax", x, 16, rows_sample=rows)
