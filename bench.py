@@ -55,15 +55,16 @@ def kernel_source_hash() -> str:
 
 
 def read_traffic():
-    """HBM bytes per launch of the dominant kernel from the committed counter summary, if it
-    was taken on the current kernel source."""
-    f = ROOT / "profiles" / "traffic_scalesweep_wmse_llama8b_layer.json"
+    """HBM bytes per launch of the dominant kernel from the committed counter summary (two
+    rocprofv3 --pmc runs, FETCH_SIZE and WRITE_SIZE, scaled by a plain copy's readings), or
+    None if the counters were taken on another version of the kernel source."""
+    f = ROOT / "profiles" / "traffic_scalesweep_wmse_llama8b_layer.txt"
     if not f.exists():
         return None
-    d = json.loads(f.read_text())
-    if d.get("kernel_source_sha256_16") != kernel_source_hash():
+    d = dict(line.split(None, 1) for line in f.read_text().splitlines() if line.strip())
+    if d.get("kernel_source_sha256_16", "").strip() != kernel_source_hash():
         return None
-    return d.get("hbm_bytes_per_launch")
+    return int(d["hbm_bytes_per_launch"])
 
 
 def main():

@@ -59,10 +59,10 @@ typedef enum {
     NVFP4_ERR_HIP = -8        /* a kernel launch failed */
 } nvfp4_status;
 
-/* Bytes of device workspace the dynamic-scale path needs (a small constant).  The workspace
- * carries the grid-wide |x| maximum and an arrival counter between the two kernels of one
- * call.  It must be zero-filled once before its first use; every call that completes leaves
- * it zero-filled again.  Static-scale calls do not touch it (it may be NULL). */
+/* Bytes of device workspace the dynamic-scale path needs (a small constant, about 1 KiB).
+ * It carries the per-workgroup |x| maxima of the reduction kernel and the resulting S and 1/S
+ * to the quantization kernel of the same call; it needs no initialization and holds nothing
+ * between calls.  Static-scale calls do not touch it (it may be NULL). */
 size_t nvfp4_workspace_bytes(void);
 
 /* Text for a status code (a static string; never NULL). */

@@ -27,9 +27,12 @@
 //    IEEE division.  RN32(y / M) then rounds to the same E2M1 value as y / M itself, because
 //    an E2M1 midpoint times M has few enough bits that a 24-bit y cannot lie within half an
 //    ulp of the quotient's midpoint without hitting it.
-//  * The dynamic global scale needs max |x| first: a streaming kernel reduces it (wave and
-//    workgroup maxima, one atomic max per workgroup) and its last workgroup forms S = amax /
-//    (6 D) and 1/S for the quantization kernel that follows on the same stream.
+//  * The dynamic global scale needs max |x| first: a streaming kernel writes one maximum per
+//    workgroup (at most 256) into the workspace, a one-wave kernel folds them into S and 1/S,
+//    and the quantization kernel reads those two words.  Kernel boundaries order the passes.
+//    Measured alternatives were slower: folding the partials in every quantization workgroup
+//    (its prologue latency), and a last-arriving-workgroup fold in the reduction kernel (an
+//    L2 write-back per workgroup for the release; with a full fence, also an L2 invalidate).
 #include <hip/hip_runtime.h>
 
 #include <float.h>
@@ -45,9 +48,12 @@ constexpr int kLaneElems = 16;
 
 enum Method { kAbsMax = 0, kFourSix = 1, kSweepMse = 2, kSweepWmse = 3 };
 
-// Workspace words (uint32): running max of |x| bit patterns, arrival counter, S, 1/S.
-constexpr int kWsAmax = 0, kWsCount = 1, kWsScale = 2, kWsRecip = 3;
-constexpr size_t kWorkspaceBytes = 256;
+// Workspace words: one |x|-maximum bit pattern per workgroup of the reduction pass, then S
+// and 1/S.
+constexpr int kMaxPartials = 256;
+constexpr int kWsScale = kMaxPartials, kWsRecip = kMaxPartials + 1;
+constexpr size_t kWorkspaceBytes = (kMaxPartials + 4) * sizeof(uint32_t);
+
 
 // Candidate band for the exact re-scoring (relative, plus an absolute floor for losses that
 // underflow binary32).
@@ -73,21 +79,33 @@ struct Scale {
     float M, rM, s, cvs;
 };
 
+// RN32(1 / (1 + b/8)) for a 3-bit significand b (the compiler folds each quotient with IEEE
+// division; a select chain keeps the table fill free of memory loads).
+__device__ __forceinline__ float recip_significand(uint32_t b) {
+    float r = 1.0f / 1.875f;
+    r = b == 6u ? 1.0f / 1.75f : r;
+    r = b == 5u ? 1.0f / 1.625f : r;
+    r = b == 4u ? 1.0f / 1.5f : r;
+    r = b == 3u ? 1.0f / 1.375f : r;
+    r = b == 2u ? 1.0f / 1.25f : r;
+    r = b == 1u ? 1.0f / 1.125f : r;
+    return b == 0u ? 1.0f : r;
+}
+
+// Fills the per-code table (threads 0..127); the caller synchronizes before reading it.
 __device__ __forceinline__ void fill_scale_table(Scale* tab) {
     const int c = threadIdx.x;
     if (c < 128) {
         const int cc = c > 126 ? 126 : c;
         const float s = e4m3_value(cc);
-        const float M = cc == 0 ? 0.f
-                                : __uint_as_float((__float_as_uint(s) & 0x007FFFFFu) | 0x3F800000u);
+        const uint32_t b = (__float_as_uint(s) >> 20) & 7u;   // s = (1 + b/8) 2^E exactly
         Scale e;
-        e.M = M;
-        e.rM = cc == 0 ? 0.f : __fdiv_rn(1.0f, M);
+        e.M = cc == 0 ? 0.f : __uint_as_float((b << 20) | 0x3F800000u);
+        e.rM = cc == 0 ? 0.f : recip_significand(b);
         e.s = s;
         e.cvs = cc == 0 ? 1.0f : s;
         tab[c] = e;
     }
-    __syncthreads();
 }
 
 __device__ __forceinline__ int clamp_code(int c) { return c < 0 ? 0 : (c > 126 ? 126 : c); }
@@ -191,6 +209,14 @@ __device__ __forceinline__ void load_weights(const float* p, float (&w)[kLaneEle
 // Block loss of one candidate scale, binary32 (fast screen).
 // ---------------------------------------------------------------------------------------
 
+// A register whose value does not matter: the FP4 conversion writes one byte of its
+// destination and keeps the other three from this operand, and only that byte is read back.
+__device__ __forceinline__ uint32_t any_bits() {
+    uint32_t v;
+    asm volatile("" : "=v"(v));
+    return v;
+}
+
 // u[i] ~ |y_i| / M (rounded once); the conversion divides by 2^E exactly and rounds to E2M1;
 // its decode gives g 2^E and e = |y| - (g 2^E) M is formed with one fused multiply-add.
 template <bool WEIGHTED>
@@ -199,7 +225,7 @@ __device__ __forceinline__ float cand_loss(const float (&u)[kLaneElems], const f
     float acc0 = 0.f, acc1 = 0.f;
 #pragma unroll
     for (int i = 0; i < kLaneElems; i += 2) {
-        const uint32_t p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, u[i], u[i + 1], cvs, 0);
+        const uint32_t p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(any_bits(), u[i], u[i + 1], cvs, 0);
         const float2v g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(p, cvs, 0);
         const float e0 = fmaf(-g.x, M, fabsf(y[i]));
         const float e1 = fmaf(-g.y, M, fabsf(y[i + 1]));
@@ -214,11 +240,14 @@ __device__ __forceinline__ float cand_loss(const float (&u)[kLaneElems], const f
     return acc0 + acc1;
 }
 
-// Exactly rounded u = RN32(v / M) for M in [1, 2) with rM = RN32(1 / M) (Markstein).
+// Exactly rounded u = RN32(v / M) for M in [1, 2) with rM = RN32(1 / M) (Markstein): the
+// remainder u M - v is exact in one fused multiply-add and corrects u once.  Written as
+// u - (u M - v) rM so that a zero quotient keeps the sign of v (-0 + -0 = -0), which the
+// nibble's sign bit needs; with M = rM = 0 (the zero scale) it returns +-0 as well.
 __device__ __forceinline__ float div_by_significand(float v, float M, float rM) {
     const float u = v * rM;
-    const float r = fmaf(-u, M, v);
-    return fmaf(r, rM, u);
+    const float r = fmaf(u, M, -v);
+    return fmaf(-r, rM, u);
 }
 
 // Exact block loss in binary64, summed in element order 0..n-1 across the block's lanes:
@@ -278,16 +307,17 @@ __device__ __forceinline__ float global_scale(uint32_t amax_bits, float denom) {
 
 template <typename In>
 __global__ __launch_bounds__(kThreads) void amax_kernel(const In* __restrict__ x, int64_t nvec,
-                                                        float denom, uint32_t* __restrict__ ws,
-                                                        float* __restrict__ tensor_scale) {
+                                                        uint32_t* __restrict__ partials) {
     const uint4* v = reinterpret_cast<const uint4*>(x);
     uint32_t m = 0;
     const int64_t stride = (int64_t)gridDim.x * kThreads;
     int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    for (; i + 3 * stride < nvec; i += 4 * stride) {
-        const uint4 a = v[i], b = v[i + stride], c = v[i + 2 * stride], d = v[i + 3 * stride];
-        m = max(m, max(max(absmax_bits(a, In()), absmax_bits(b, In())),
-                       max(absmax_bits(c, In()), absmax_bits(d, In()))));
+    for (; i + 7 * stride < nvec; i += 8 * stride) {
+        uint4 d[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) d[k] = v[i + k * stride];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) m = max(m, absmax_bits(d[k], In()));
     }
     for (; i < nvec; i += stride) m = max(m, absmax_bits(v[i], In()));
 #pragma unroll
@@ -295,22 +325,22 @@ __global__ __launch_bounds__(kThreads) void amax_kernel(const In* __restrict__ x
     __shared__ uint32_t part[kThreads / 64];
     if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;
     __syncthreads();
+    if (threadIdx.x == 0) partials[blockIdx.x] = max(max(part[0], part[1]), max(part[2], part[3]));
+}
+
+// Folds the per-workgroup maxima into S and 1/S (one wave): S goes to the caller's output
+// and, with 1/S, to the workspace words after the partials, for the quantization kernel.
+__global__ __launch_bounds__(64) void scale_kernel(uint32_t* __restrict__ ws, int npart,
+                                                   float denom, float* __restrict__ tensor_scale) {
+    uint32_t m = 0;
+    for (int i = threadIdx.x; i < npart; i += 64) m = max(m, ws[i]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off, 64));
     if (threadIdx.x == 0) {
-        m = max(max(part[0], part[1]), max(part[2], part[3]));
-        atomicMax(&ws[kWsAmax], m);
-        __threadfence();
-        const uint32_t arrived = atomicAdd(&ws[kWsCount], 1u);
-        if (arrived == gridDim.x - 1) {            // the last workgroup finalizes and resets
-            __threadfence();
-            const uint32_t bits = atomicAdd(&ws[kWsAmax], 0u);
-            const float S = global_scale(bits, denom);
-            const float rS = __fdiv_rn(1.0f, S);
-            tensor_scale[0] = S;
-            ws[kWsScale] = __float_as_uint(S);
-            ws[kWsRecip] = __float_as_uint(rS);
-            ws[kWsAmax] = 0u;
-            ws[kWsCount] = 0u;
-        }
+        const float S = global_scale(m, denom);
+        tensor_scale[0] = S;
+        ws[kWsScale] = __float_as_uint(S);
+        ws[kWsRecip] = __float_as_uint(__fdiv_rn(1.0f, S));
     }
 }
 
@@ -325,10 +355,10 @@ struct Params {
     uint32_t bpr;             // micro-blocks per row
     uint32_t bpr_magic;       // blk / bpr = (umulhi(blk, magic) + ((blk - hi) >> 1)) >> (shift - 1)
     uint32_t bpr_shift;
-    int dynamic;              // S, 1/S from the workspace (written by amax_kernel)
+    int dynamic;              // S, 1/S from the workspace (else given)
     float S, rS;              // static global scale and its reciprocal
-    const uint32_t* ws;
-    float* tensor_scale;      // static path: written once
+    const uint32_t* ws;       // workspace of the dynamic path
+    float* tensor_scale;      // static path: written once, by the first lane of the grid
 };
 
 __device__ __forceinline__ uint32_t div_bpr(uint32_t n, const Params& p) {
@@ -354,39 +384,17 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
     constexpr int LPB = N / kLaneElems;
     constexpr bool WEIGHTED_OBJ = METHOD == kSweepWmse || METHOD == kFourSix;
     __shared__ Scale tab[128];
-    fill_scale_table(tab);
-
+    const int lane = threadIdx.x & 63;
     const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const int64_t blk = gtid / LPB;
     const int part = (int)(gtid % LPB);
-    const int lane = threadIdx.x & 63;
     const int group_base = lane - part;
     const bool active = blk < p.nblocks;
     const int64_t blk_c = active ? blk : 0;   // inactive lanes run on block 0, store nothing
 
-    float S, rS;
-    if (p.dynamic) {
-        S = __uint_as_float(p.ws[kWsScale]);
-        rS = __uint_as_float(p.ws[kWsRecip]);
-    } else {
-        S = p.S;
-        rS = p.rS;
-        if (gtid == 0) p.tensor_scale[0] = S;
-    }
-    const bool fast_div = S >= 0x1p-26f && S <= 0x1p26f;
-
-    // ---- load and normalize y = RN32(x / S) -------------------------------------------
+    // The tile's loads go out first; the table fill and the global-scale fold overlap them.
     float y[kLaneElems];
     Loader<In>::load(x + blk_c * N + part * kLaneElems, y);
-#pragma unroll
-    for (int i = 0; i < kLaneElems; ++i) {
-        const float xv = y[i];
-        if (fast_div && fabsf(xv) >= 0x1p-74f) {
-            y[i] = div_by_significand(xv, S, rS);    // exact for these ranges (Markstein)
-        } else {
-            y[i] = __fdiv_rn(xv, S);
-        }
-    }
     float w[kLaneElems];
     const bool use_w = WEIGHTED_OBJ && colw != nullptr;
     if (use_w) {
@@ -397,7 +405,30 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
 #pragma unroll
         for (int i = 0; i < kLaneElems; ++i) w[i] = 1.0f;
     }
+    fill_scale_table(tab);
+    __syncthreads();
+    float S, rS;
+    if (p.dynamic) {      // formed by scale_kernel, earlier on the same stream
+        S = __uint_as_float(p.ws[kWsScale]);
+        rS = __uint_as_float(p.ws[kWsRecip]);
+    } else {
+        S = p.S;
+        rS = p.rS;
+        if (blockIdx.x == 0 && threadIdx.x == 0) p.tensor_scale[0] = S;
+    }
+    const bool fast_div = S >= 0x1p-26f && S <= 0x1p26f;
 
+    {
+    // ---- normalize y = RN32(x / S) -----------------------------------------------------
+#pragma unroll
+    for (int i = 0; i < kLaneElems; ++i) {
+        const float xv = y[i];
+        if (fast_div && fabsf(xv) >= 0x1p-74f) {
+            y[i] = div_by_significand(xv, S, rS);    // exact for these ranges (Markstein)
+        } else {
+            y[i] = __fdiv_rn(xv, S);
+        }
+    }
     float ymax = 0.f;
 #pragma unroll
     for (int i = 0; i < kLaneElems; ++i) ymax = fmaxf(ymax, fabsf(y[i]));
@@ -513,9 +544,7 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
         float u[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            const float v = y[8 * h + i];
-            const float t = div_by_significand(v, sc.M, sc.rM);
-            u[i] = __uint_as_float((__float_as_uint(t) & 0x7FFFFFFFu) | (__float_as_uint(v) & 0x80000000u));
+            u[i] = div_by_significand(y[8 * h + i], sc.M, sc.rM);
         }
         uint32_t r = 0u;
         r = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(r, u[0], u[1], sc.cvs, 0);
@@ -528,6 +557,7 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
         uint2* dst = reinterpret_cast<uint2*>(q + ((blk * N + part * kLaneElems) >> 1));
         *dst = make_uint2(packed[0], packed[1]);
         if (part == 0) scales[blk] = (uint8_t)code;
+    }
     }
 }
 
@@ -607,7 +637,7 @@ template <int METHOD, typename In, int N>
 hipError_t launch_quant(const Call& c, const Params& p) {
     constexpr int LPB = N / kLaneElems;
     const int64_t lanes = p.nblocks * LPB;
-    const int64_t grid = (lanes + kThreads - 1) / kThreads;
+    const int64_t grid = (lanes + kThreads - 1) / kThreads;   // one workgroup per tile
     hipLaunchKernelGGL((quant_kernel<METHOD, In, N>), dim3((unsigned)grid), dim3(kThreads), 0, c.stream,
                        static_cast<const In*>(c.x), c.colw, c.q, c.scales, p);
     return hipGetLastError();
@@ -652,27 +682,31 @@ int run_quant(const Call& c) {
 
     hipError_t err = hipSuccess;
     const float denom = 6.0f * c.fp8_range;
+    if (nblocks == 0) {       // nothing to quantize: S of an empty tensor is 1 (or the given S)
+        hipLaunchKernelGGL(write_scale_kernel, dim3(1), dim3(1), 0, c.stream, c.tensor_scale,
+                           dynamic ? 1.0f : c.static_scale);
+        return hipGetLastError() == hipSuccess ? NVFP4_OK : NVFP4_ERR_HIP;
+    }
+    int64_t g = 0;
     if (dynamic) {
         const int64_t nvec = n * (c.dtype == NVFP4_IN_F32 ? 4 : 2) / 16;
-        int64_t g = (nvec + kThreads * 4 - 1) / (kThreads * 4);
+        g = (nvec + kThreads * 8 - 1) / (kThreads * 8);
         if (g < 1) g = 1;
-        if (g > 2048) g = 2048;
+        if (g > kMaxPartials) g = kMaxPartials;
         if (c.dtype == NVFP4_IN_F32)
             hipLaunchKernelGGL(amax_kernel<float>, dim3((unsigned)g), dim3(kThreads), 0, c.stream,
-                               static_cast<const float*>(c.x), nvec, denom,
-                               static_cast<uint32_t*>(c.ws), c.tensor_scale);
+                               static_cast<const float*>(c.x), nvec, static_cast<uint32_t*>(c.ws));
         else
             hipLaunchKernelGGL(amax_kernel<uint16_t>, dim3((unsigned)g), dim3(kThreads), 0, c.stream,
-                               static_cast<const uint16_t*>(c.x), nvec, denom,
-                               static_cast<uint32_t*>(c.ws), c.tensor_scale);
+                               static_cast<const uint16_t*>(c.x), nvec, static_cast<uint32_t*>(c.ws));
         err = hipGetLastError();
-    } else if (nblocks == 0) {
-        hipLaunchKernelGGL(write_scale_kernel, dim3(1), dim3(1), 0, c.stream, c.tensor_scale,
-                           c.static_scale);
-        err = hipGetLastError();
+        if (err == hipSuccess) {
+            hipLaunchKernelGGL(scale_kernel, dim3(1), dim3(64), 0, c.stream,
+                               static_cast<uint32_t*>(c.ws), (int)g, denom, c.tensor_scale);
+            err = hipGetLastError();
+        }
     }
     if (err != hipSuccess) return NVFP4_ERR_HIP;
-    if (nblocks == 0) return NVFP4_OK;
 
     Params p;
     p.nblocks = nblocks;
