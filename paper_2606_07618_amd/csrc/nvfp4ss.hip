@@ -92,18 +92,31 @@ __device__ __forceinline__ float recip_significand(uint32_t b) {
     return b == 0u ? 1.0f : r;
 }
 
-// Fills the per-code table (threads 0..127); the caller synchronizes before reading it.
+// The table covers codes -16..143 so that a window's candidates index it without clamping.
+// Codes that are not candidates get NaN in M, rM and cvs, so their loss comes out NaN and
+// loses every comparison: codes outside 0..126, and code 0 unless the zero scale is allowed
+// (AbsMax and 4/6 may pick it; a ScaleSweep window starts at code 1).
+constexpr int kTabLo = 16, kTabSize = 160;
+
+// Fills the table (threads 0..159 write entry threadIdx.x - 16); the caller synchronizes
+// before reading it.
+template <bool ZERO_SCALE>
 __device__ __forceinline__ void fill_scale_table(Scale* tab) {
-    const int c = threadIdx.x;
-    if (c < 128) {
-        const int cc = c > 126 ? 126 : c;
-        const float s = e4m3_value(cc);
-        const uint32_t b = (__float_as_uint(s) >> 20) & 7u;   // s = (1 + b/8) 2^E exactly
+    const int c = (int)threadIdx.x - kTabLo;
+    if (c < kTabSize - kTabLo) {
+        const float nan = __uint_as_float(0x7FC00000u);
         Scale e;
-        e.M = cc == 0 ? 0.f : __uint_as_float((b << 20) | 0x3F800000u);
-        e.rM = cc == 0 ? 0.f : recip_significand(b);
-        e.s = s;
-        e.cvs = cc == 0 ? 1.0f : s;
+        if (c < 0 || c > 126) {
+            e.M = e.rM = e.s = e.cvs = nan;
+        } else {
+            const float s = e4m3_value(c);
+            const uint32_t b = (__float_as_uint(s) >> 20) & 7u;   // s = (1 + b/8) 2^E exactly
+            const bool zero = c == 0;
+            e.M = zero ? (ZERO_SCALE ? 0.f : nan) : __uint_as_float((b << 20) | 0x3F800000u);
+            e.rM = zero ? (ZERO_SCALE ? 0.f : nan) : recip_significand(b);
+            e.s = s;
+            e.cvs = zero ? (ZERO_SCALE ? 1.0f : nan) : s;
+        }
         tab[c] = e;
     }
 }
@@ -383,7 +396,8 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
                                                          uint8_t* __restrict__ scales, Params p) {
     constexpr int LPB = N / kLaneElems;
     constexpr bool WEIGHTED_OBJ = METHOD == kSweepWmse || METHOD == kFourSix;
-    __shared__ Scale tab[128];
+    __shared__ Scale tab_all[kTabSize];
+    Scale* tab = tab_all + kTabLo;                 // tab[c] for codes c in -16..143
     const int lane = threadIdx.x & 63;
     const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const int64_t blk = gtid / LPB;
@@ -405,7 +419,7 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
 #pragma unroll
         for (int i = 0; i < kLaneElems; ++i) w[i] = 1.0f;
     }
-    fill_scale_table(tab);
+    fill_scale_table<METHOD == kAbsMax || METHOD == kFourSix>(tab);
     __syncthreads();
     float S, rS;
     if (p.dynamic) {      // formed by scale_kernel, earlier on the same stream
@@ -475,30 +489,27 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
             // normal codes only: c, c+8, c+16 share the significand M and differ in 2^E
 #pragma unroll
             for (int d = 0; d < 8 && d < NC; ++d) {
-                const Scale s0 = tab[clamp_code(cb + d)];
+                const Scale s0 = tab[cb + d];
                 float u[kLaneElems];
 #pragma unroll
                 for (int i = 0; i < kLaneElems; ++i) u[i] = fabsf(y[i]) * s0.rM;
 #pragma unroll
                 for (int j = d; j < NC; j += 8) {
-                    const Scale sj = tab[clamp_code(cb + j)];
+                    const Scale sj = tab[cb + j];
                     J[j] = group_sum<LPB>(cand_loss<WGT>(u, y, w, sj.cvs, sj.M));
                 }
             }
         } else {
 #pragma unroll
             for (int d = 0; d < NC; ++d) {
-                const Scale sd = tab[clamp_code(cb + d)];
+                const Scale sd = tab[cb + d];
                 float u[kLaneElems];
 #pragma unroll
                 for (int i = 0; i < kLaneElems; ++i) u[i] = fabsf(y[i]) * sd.rM;
                 J[d] = group_sum<LPB>(cand_loss<WGT>(u, y, w, sd.cvs, sd.M));
             }
         }
-        // codes outside 1..126 are not candidates
-#pragma unroll
-        for (int d = 0; d < NC; ++d)
-            if (cb + d < 1 || cb + d > 126) J[d] = __uint_as_float(0x7F800000u);
+        // (codes outside 1..126 scored NaN through their table entries)
         // argmin on the loss with its 7 low bits replaced by the candidate index: exact
         // ordering except between losses within 2^-16 of each other, which the band re-scores
         uint32_t best = 0xFFFFFFFFu;
