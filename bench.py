@@ -2,11 +2,12 @@
 """Benchmark of the NVFP4 ScaleSweep hot path on one MI355X.
 
 One step quantizes every weight of a Llama-3-8B-shaped decoder layer (bfloat16, block 16,
-dynamic global scale with D = 256) with ScaleSweep under both objectives, MSE and WMSE: for
-each of the 7 tensors the amax pass and the sweep kernel, twice.  `value` is the bfloat16
-input consumed per second (both objectives read the layer).  The line also carries:
+dynamic global scale with D = 256) with ScaleSweep under both objectives, MSE and WMSE: one
+batched call per objective over the layer's 7 tensors (each tensor's |x| reduction on a side
+stream, overlapped with the previous tensor's sweep).  `value` is the bfloat16 input consumed
+per second (both objectives read the layer).  The line also carries:
   * per-method GB/s of the same GPU's AbsMax (D = 448), 4/6 and each ScaleSweep objective,
-    and ScaleSweep's time relative to AbsMax;
+    batched over the layer and as 7 single-tensor calls, and the time relative to AbsMax;
   * `roofline` for the dominant kernel (the WMSE sweep kernel), from HIP events around its
     launches on the stream it runs on;
   * `cpu_baseline`: the oracle on the host, single-threaded, on a bounded sample.
@@ -97,15 +98,22 @@ def main():
     outs = {m: [alloc(x) for x in xs] for m in
             ("absmax", "four_over_six", "scalesweep_mse", "scalesweep_wmse")}
 
+    bws = torch.empty(nv.nvfp4_batched_workspace_bytes(len(xs)) // 4, dtype=torch.int32,
+                      device=dev)
+
     def run(method, static=None):
         for i, x in enumerate(xs):
             w = ws_col[i] if method in ("scalesweep_wmse",) else None
             nv.quantize(x, method, 16, weight=w, ws=ws, out=outs[method][i],
                         static_scale=0.0 if static is None else static[i])
 
+    def run_batched(method):
+        nv.quantize_batched(xs, method, 16, weights=ws_col if method == "scalesweep_wmse" else None,
+                            ws=bws, outs=outs[method])
+
     def step():
-        run("scalesweep_mse")
-        run("scalesweep_wmse")
+        run_batched("scalesweep_mse")
+        run_batched("scalesweep_wmse")
 
     for _ in range(args.warmup):
         step()
@@ -120,19 +128,19 @@ def main():
 
     # ---- per-method throughput (events on the current stream, which the library uses) ----
     reps = max(5, args.steps // 2)
-    per_method = {}
+    per_method, per_method_single = {}, {}
     for m in ("absmax", "four_over_six", "scalesweep_mse", "scalesweep_wmse"):
-        run(m)
-        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        ev0.record()
-        for _ in range(reps):
-            run(m)
-        ev1.record()
-        torch.cuda.synchronize()
-        ms = ev0.elapsed_time(ev1) / reps
-        per_method[m] = {"ms_per_layer": round(ms, 4),
-                         "input_GBps": round(in_bytes / ms / 1e6, 1),
-                         "Gelem_per_s": round(n_elem / ms / 1e6, 2)}
+        for table, fn in ((per_method, run_batched), (per_method_single, run)):
+            fn(m)
+            torch.cuda.synchronize()
+            t_a = time.perf_counter()
+            for _ in range(reps):
+                fn(m)
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t_a) * 1e3 / reps
+            table[m] = {"ms_per_layer": round(ms, 4),
+                        "input_GBps": round(in_bytes / ms / 1e6, 1),
+                        "Gelem_per_s": round(n_elem / ms / 1e6, 2)}
     overhead = {m: round(per_method[m]["ms_per_layer"] / per_method["absmax"]["ms_per_layer"], 3)
                 for m in ("four_over_six", "scalesweep_mse", "scalesweep_wmse")}
 
@@ -209,10 +217,12 @@ def main():
         "config": {"workload": "llama3_8b_decoder_layer_weights_bf16", "tensors": {
             n: list(x.shape) for n, x in zip(names, xs)}, "elements": n_elem, "block": 16,
             "objectives": ["scalesweep_mse", "scalesweep_wmse"],
-            "global_scale": "dynamic, S = amax / (6 * 256)", "value_counts": "bf16 input bytes of both objectives"},
+            "global_scale": "dynamic, S = amax / (6 * 256)", "value_counts": "bf16 input bytes of both objectives",
+            "calls": "nvfp4_quant_batched over the 7 tensors, one call per objective"},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "per_method": per_method,
+        "per_method_single_calls": per_method_single,
         "time_vs_absmax": overhead,
     }
     print(json.dumps(line))

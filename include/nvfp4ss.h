@@ -123,6 +123,37 @@ int nvfp4_quant_scalesweep_wmse(const void* x, int dtype, int64_t rows, int64_t 
                                 float* tensor_scale, uint8_t* q, uint8_t* scales,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
+/* One tensor of a batched call: device pointers and shape, as in the single-tensor calls
+ * (col_weight: NULL unless the method uses weights). */
+typedef struct {
+    const void* x;
+    int64_t rows, cols;
+    const float* col_weight;
+    float* tensor_scale;
+    uint8_t* q;
+    uint8_t* scales;
+} nvfp4_tensor;
+
+/* Workspace bytes for a batched call over `count` tensors (count single-call workspaces). */
+size_t nvfp4_batched_workspace_bytes(int count);
+
+/* Quantizes `count` tensors with one method (0 AbsMax, 1 4/6, 2 ScaleSweep-MSE,
+ * 3 ScaleSweep-WMSE), each with its own dynamic global scale: the per-tensor round-to-nearest
+ * pipeline of the experiment setup applied to, e.g., the weights of one decoder layer.  Every
+ * tensor's outputs are bit-identical to its single-tensor call.  `tensors` is a host array;
+ * the descriptors may be reused once the call returns.  The |x| reductions run on
+ * `side_stream` and the quantization kernels on `stream`, ordered by events: the largest
+ * tensor is reduced and quantized first, and the other tensors' bandwidth-bound reductions
+ * overlap its arithmetic-bound sweep; side_stream == NULL or == stream runs everything on
+ * `stream`.  Both streams must be of
+ * default priority.  On return the work of both streams is ordered before any later work
+ * enqueued on `stream`.  workspace: >= nvfp4_batched_workspace_bytes(count), 16-byte
+ * aligned, no initialization.  Errors as for the single-tensor calls (validated for every
+ * tensor before any launch); count < 0 or an unknown method: NVFP4_ERR_ARG. */
+int nvfp4_quant_batched(int method, const nvfp4_tensor* tensors, int count, int dtype, int block,
+                        float fp8_range, void* workspace, size_t workspace_bytes, void* stream,
+                        void* side_stream);
+
 /* Reconstruction x_hat_i = q_i * s_{block(i)} * S (NVFP4 Quantization section) into out
  * [rows, cols] binary32 (out_dtype must be NVFP4_IN_F32): q * s is exact, so each output is the
  * single rounding RN32((q * s) * S).  tensor_scale is read from device memory. */

@@ -10,7 +10,9 @@ from .nvfp4 import (  # noqa: F401
     NVFP4Error,
     dequant,
     lib,
+    nvfp4_batched_workspace_bytes,
     nvfp4_dequant,
+    nvfp4_quant_batched,
     nvfp4_quant_absmax,
     nvfp4_quant_four_over_six,
     nvfp4_quant_scalesweep_mse,
@@ -18,5 +20,6 @@ from .nvfp4 import (  # noqa: F401
     nvfp4_status_string,
     nvfp4_workspace_bytes,
     quantize,
+    quantize_batched,
     workspace,
 )

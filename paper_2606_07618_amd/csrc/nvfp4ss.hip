@@ -670,7 +670,8 @@ hipError_t launch_quant_m(const Call& c, const Params& p) {
                                    : launch_quant_n<METHOD, uint16_t>(c, p);
 }
 
-int run_quant(const Call& c) {
+// Synchronous argument checks shared by every entry point; nothing is launched.
+int validate(const Call& c) {
     if (!c.tensor_scale) return NVFP4_ERR_NULL;
     if (c.dtype != NVFP4_IN_F32 && c.dtype != NVFP4_IN_BF16) return NVFP4_ERR_DTYPE;
     if (!valid_block(c.block)) return NVFP4_ERR_BLOCK;
@@ -680,47 +681,43 @@ int run_quant(const Call& c) {
     if (c.method == kSweepWmse && !c.colw) return NVFP4_ERR_NULL;
     const int64_t n = c.rows * c.cols;
     if (n > 0 && (!c.x || !c.q || !c.scales)) return NVFP4_ERR_NULL;
-    const bool dynamic = c.static_scale == 0.0f;
-    if (dynamic) {
+    if (c.static_scale == 0.0f) {
         if (!c.ws) return NVFP4_ERR_WORKSPACE;
         if (c.ws_bytes < kWorkspaceBytes) return NVFP4_ERR_WORKSPACE;
         if (!aligned(c.ws, 16)) return NVFP4_ERR_ALIGN;
     }
     if (n > 0 && (!aligned(c.x, 16) || !aligned(c.q, 8))) return NVFP4_ERR_ALIGN;
     if (c.colw && !aligned(c.colw, 16)) return NVFP4_ERR_ALIGN;
-    const int64_t nblocks = n / c.block;
-    if (nblocks > 0x7FFFFFFFLL) return NVFP4_ERR_SHAPE;     // 32-bit block indexing
+    if (n / c.block > 0x7FFFFFFFLL) return NVFP4_ERR_SHAPE;     // 32-bit block indexing
+    return NVFP4_OK;
+}
 
-    hipError_t err = hipSuccess;
-    const float denom = 6.0f * c.fp8_range;
-    if (nblocks == 0) {       // nothing to quantize: S of an empty tensor is 1 (or the given S)
-        hipLaunchKernelGGL(write_scale_kernel, dim3(1), dim3(1), 0, c.stream, c.tensor_scale,
-                           dynamic ? 1.0f : c.static_scale);
-        return hipGetLastError() == hipSuccess ? NVFP4_OK : NVFP4_ERR_HIP;
-    }
-    int64_t g = 0;
-    if (dynamic) {
-        const int64_t nvec = n * (c.dtype == NVFP4_IN_F32 ? 4 : 2) / 16;
-        g = (nvec + kThreads * 8 - 1) / (kThreads * 8);
-        if (g < 1) g = 1;
-        if (g > kMaxPartials) g = kMaxPartials;
-        if (c.dtype == NVFP4_IN_F32)
-            hipLaunchKernelGGL(amax_kernel<float>, dim3((unsigned)g), dim3(kThreads), 0, c.stream,
-                               static_cast<const float*>(c.x), nvec, static_cast<uint32_t*>(c.ws));
-        else
-            hipLaunchKernelGGL(amax_kernel<uint16_t>, dim3((unsigned)g), dim3(kThreads), 0, c.stream,
-                               static_cast<const uint16_t*>(c.x), nvec, static_cast<uint32_t*>(c.ws));
-        err = hipGetLastError();
-        if (err == hipSuccess) {
-            hipLaunchKernelGGL(scale_kernel, dim3(1), dim3(64), 0, c.stream,
-                               static_cast<uint32_t*>(c.ws), (int)g, denom, c.tensor_scale);
-            err = hipGetLastError();
-        }
-    }
-    if (err != hipSuccess) return NVFP4_ERR_HIP;
+// Dynamic global scale of a non-empty tensor: the |x| reduction and the fold into S, 1/S.
+hipError_t launch_scale(const Call& c, hipStream_t stream, int* npart) {
+    const int64_t n = c.rows * c.cols;
+    const int64_t nvec = n * (c.dtype == NVFP4_IN_F32 ? 4 : 2) / 16;
+    int64_t g = (nvec + kThreads * 8 - 1) / (kThreads * 8);
+    if (g < 1) g = 1;
+    if (g > kMaxPartials) g = kMaxPartials;
+    *npart = (int)g;
+    if (c.dtype == NVFP4_IN_F32)
+        hipLaunchKernelGGL(amax_kernel<float>, dim3((unsigned)g), dim3(kThreads), 0, stream,
+                           static_cast<const float*>(c.x), nvec, static_cast<uint32_t*>(c.ws));
+    else
+        hipLaunchKernelGGL(amax_kernel<uint16_t>, dim3((unsigned)g), dim3(kThreads), 0, stream,
+                           static_cast<const uint16_t*>(c.x), nvec, static_cast<uint32_t*>(c.ws));
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(scale_kernel, dim3(1), dim3(64), 0, stream, static_cast<uint32_t*>(c.ws),
+                       (int)g, 6.0f * c.fp8_range, c.tensor_scale);
+    return hipGetLastError();
+}
 
+// The quantization kernel of a non-empty tensor (after launch_scale for a dynamic scale).
+hipError_t launch_main(const Call& c, hipStream_t stream) {
+    const bool dynamic = c.static_scale == 0.0f;
     Params p;
-    p.nblocks = nblocks;
+    p.nblocks = c.rows * c.cols / c.block;
     p.bpr = (uint32_t)(c.cols / c.block);
     make_divider(p.bpr, &p.bpr_magic, &p.bpr_shift);
     p.dynamic = dynamic ? 1 : 0;
@@ -728,13 +725,90 @@ int run_quant(const Call& c) {
     p.rS = dynamic ? 0.0f : 1.0f / c.static_scale;
     p.ws = static_cast<const uint32_t*>(c.ws);
     p.tensor_scale = c.tensor_scale;
+    Call cs = c;
+    cs.stream = stream;
     switch (c.method) {
-        case kAbsMax: err = launch_quant_m<kAbsMax>(c, p); break;
-        case kFourSix: err = launch_quant_m<kFourSix>(c, p); break;
-        case kSweepMse: err = launch_quant_m<kSweepMse>(c, p); break;
-        default: err = launch_quant_m<kSweepWmse>(c, p); break;
+        case kAbsMax: return launch_quant_m<kAbsMax>(cs, p);
+        case kFourSix: return launch_quant_m<kFourSix>(cs, p);
+        case kSweepMse: return launch_quant_m<kSweepMse>(cs, p);
+        default: return launch_quant_m<kSweepWmse>(cs, p);
     }
-    return err == hipSuccess ? NVFP4_OK : NVFP4_ERR_HIP;
+}
+
+// S of an empty tensor is 1 (or the given S).
+hipError_t launch_empty(const Call& c, hipStream_t stream) {
+    hipLaunchKernelGGL(write_scale_kernel, dim3(1), dim3(1), 0, stream, c.tensor_scale,
+                       c.static_scale == 0.0f ? 1.0f : c.static_scale);
+    return hipGetLastError();
+}
+
+int run_quant(const Call& c) {
+    const int rc = validate(c);
+    if (rc != NVFP4_OK) return rc;
+    if (c.rows * c.cols == 0) return launch_empty(c, c.stream) == hipSuccess ? NVFP4_OK : NVFP4_ERR_HIP;
+    int npart = 0;
+    if (c.static_scale == 0.0f && launch_scale(c, c.stream, &npart) != hipSuccess) return NVFP4_ERR_HIP;
+    return launch_main(c, c.stream) == hipSuccess ? NVFP4_OK : NVFP4_ERR_HIP;
+}
+
+// Several tensors, dynamic scales.  The largest tensor goes first: its reduction, then (main
+// stream) its quantization kernel; meanwhile the side stream reduces all the other tensors,
+// and the main stream waits once for that before quantizing them back to back.  So the
+// bandwidth-bound reductions overlap the arithmetic-bound sweep of the largest tensor, and
+// the main stream carries two event waits in all (each wait costs a few microseconds even
+// when its event has long completed).
+int run_batched(int method, const nvfp4_tensor* t, int count, int dtype, int block,
+                float fp8_range, void* ws, size_t ws_bytes, hipStream_t main, hipStream_t side) {
+    if (count < 0) return NVFP4_ERR_ARG;
+    if (count > 0 && !t) return NVFP4_ERR_NULL;
+    if (method < kAbsMax || method > kSweepWmse) return NVFP4_ERR_ARG;
+    if (count > 0 && (!ws || ws_bytes < (size_t)count * kWorkspaceBytes)) return NVFP4_ERR_WORKSPACE;
+    if (count > 0 && !aligned(ws, 16)) return NVFP4_ERR_ALIGN;
+    auto call_of = [&](int k) {
+        return Call{method, t[k].x, dtype, t[k].rows, t[k].cols, block, t[k].col_weight,
+                    fp8_range, 0.0f, t[k].tensor_scale, t[k].q, t[k].scales,
+                    static_cast<char*>(ws) + (size_t)k * kWorkspaceBytes, kWorkspaceBytes, main};
+    };
+    int first = -1;
+    int64_t first_n = -1;
+    for (int k = 0; k < count; ++k) {
+        const int rc = validate(call_of(k));
+        if (rc != NVFP4_OK) return rc;
+        if (t[k].rows * t[k].cols > first_n) {
+            first_n = t[k].rows * t[k].cols;
+            first = k;
+        }
+    }
+    if (count == 0) return NVFP4_OK;
+    if (side == main) side = nullptr;
+    hipStream_t red = side ? side : main;
+    hipEvent_t ev[3] = {nullptr, nullptr, nullptr};   // main ready, first reduced, rest reduced
+    bool ok = true;
+    if (side) {
+        for (int e = 0; ok && e < 3; ++e) ok = hipEventCreateWithFlags(&ev[e], hipEventDisableTiming) == hipSuccess;
+        // the reductions start after the work already queued on the main stream
+        ok = ok && hipEventRecord(ev[0], main) == hipSuccess && hipStreamWaitEvent(side, ev[0], 0) == hipSuccess;
+    }
+    int npart = 0;
+    const Call cf = call_of(first);
+    if (ok && first_n > 0) ok = launch_scale(cf, red, &npart) == hipSuccess;
+    if (ok && side) ok = hipEventRecord(ev[1], side) == hipSuccess && hipStreamWaitEvent(main, ev[1], 0) == hipSuccess;
+    if (ok) ok = (first_n > 0 ? launch_main(cf, main) : launch_empty(cf, main)) == hipSuccess;
+    bool any_rest = false;
+    for (int k = 0; ok && k < count; ++k) {
+        if (k == first || t[k].rows * t[k].cols == 0) continue;
+        ok = launch_scale(call_of(k), red, &npart) == hipSuccess;
+        any_rest = true;
+    }
+    if (ok && side && any_rest) ok = hipEventRecord(ev[2], side) == hipSuccess && hipStreamWaitEvent(main, ev[2], 0) == hipSuccess;
+    for (int k = 0; ok && k < count; ++k) {
+        if (k == first) continue;
+        const Call c = call_of(k);
+        ok = (c.rows * c.cols > 0 ? launch_main(c, main) : launch_empty(c, main)) == hipSuccess;
+    }
+    for (int e = 0; e < 3; ++e)      // events may be destroyed while pending
+        if (ev[e]) hipEventDestroy(ev[e]);
+    return ok ? NVFP4_OK : NVFP4_ERR_HIP;
 }
 
 }  // namespace
@@ -742,6 +816,17 @@ int run_quant(const Call& c) {
 extern "C" {
 
 size_t nvfp4_workspace_bytes(void) { return kWorkspaceBytes; }
+
+size_t nvfp4_batched_workspace_bytes(int count) {
+    return count > 0 ? (size_t)count * kWorkspaceBytes : 0;
+}
+
+int nvfp4_quant_batched(int method, const nvfp4_tensor* tensors, int count, int dtype, int block,
+                        float fp8_range, void* workspace, size_t workspace_bytes, void* stream,
+                        void* side_stream) {
+    return run_batched(method, tensors, count, dtype, block, fp8_range, workspace,
+                       workspace_bytes, (hipStream_t)stream, (hipStream_t)side_stream);
+}
 
 const char* nvfp4_status_string(int status) {
     switch (status) {

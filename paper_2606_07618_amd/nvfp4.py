@@ -35,6 +35,8 @@ def _load():
     quant_w = [P, I, I64, I64, I, P, F, F, P, P, P, P, SZ, P]
     sigs = {
         "nvfp4_workspace_bytes": (SZ, []),
+        "nvfp4_batched_workspace_bytes": (SZ, [I]),
+        "nvfp4_quant_batched": (I, [I, P, I, I, I, F, P, SZ, P, P]),
         "nvfp4_status_string": (ctypes.c_char_p, [I]),
         "nvfp4_quant_absmax": (I, quant),
         "nvfp4_quant_four_over_six": (I, quant_w),
@@ -49,6 +51,13 @@ def _load():
     return L
 
 
+class NVFP4Tensor(ctypes.Structure):
+    """The C struct nvfp4_tensor."""
+    _fields_ = [("x", ctypes.c_void_p), ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("col_weight", ctypes.c_void_p), ("tensor_scale", ctypes.c_void_p),
+                ("q", ctypes.c_void_p), ("scales", ctypes.c_void_p)]
+
+
 lib = _load()
 
 # The C entry points, under the header's names.
@@ -59,6 +68,9 @@ nvfp4_quant_four_over_six = lib.nvfp4_quant_four_over_six
 nvfp4_quant_scalesweep_mse = lib.nvfp4_quant_scalesweep_mse
 nvfp4_quant_scalesweep_wmse = lib.nvfp4_quant_scalesweep_wmse
 nvfp4_dequant = lib.nvfp4_dequant
+nvfp4_batched_workspace_bytes = lib.nvfp4_batched_workspace_bytes
+nvfp4_quant_batched = lib.nvfp4_quant_batched
+METHOD_IDS = {"absmax": 0, "four_over_six": 1, "scalesweep_mse": 2, "scalesweep_wmse": 3}
 
 
 def _ptr(t):
@@ -70,9 +82,9 @@ def _stream(device):
 
 
 def workspace(device) -> torch.Tensor:
-    """A zero-filled workspace for the dynamic-scale path (reusable by sequential calls on
-    one stream; every call leaves it zero-filled again)."""
-    return torch.zeros(nvfp4_workspace_bytes() // 4, dtype=torch.int32, device=device)
+    """A workspace for the dynamic-scale path (no initialization needed; reusable by calls
+    that are ordered on one stream)."""
+    return torch.empty(nvfp4_workspace_bytes() // 4, dtype=torch.int32, device=device)
 
 
 def quantize(x: torch.Tensor, method: str = "scalesweep_wmse", block: int = 16,
@@ -126,6 +138,54 @@ def quantize(x: torch.Tensor, method: str = "scalesweep_wmse", block: int = 16,
     if rc != 0:
         raise NVFP4Error(rc, f"nvfp4_quant_{method}")
     return q, sc, S
+
+
+_side_streams = {}
+
+
+def side_stream(device) -> torch.cuda.Stream:
+    """A default-priority stream per device for the batched call's reductions."""
+    key = torch.device(device).index or 0
+    if key not in _side_streams:
+        _side_streams[key] = torch.cuda.Stream(device=device)
+    return _side_streams[key]
+
+
+def quantize_batched(xs, method: str = "scalesweep_wmse", block: int = 16, weights=None,
+                     fp8_range: float | None = None, ws: torch.Tensor | None = None,
+                     outs=None, overlap: bool = True):
+    """Quantize a list of 2-D device tensors (one dtype) with one method and a dynamic global
+    scale each, in one batched call.  Returns a list of (q, scales, S)."""
+    if not xs:
+        return []
+    dev = xs[0].device
+    dt = BF16 if xs[0].dtype == torch.bfloat16 else F32
+    D = DEFAULT_RANGE[method] if fp8_range is None else float(fp8_range)
+    weights = weights or [None] * len(xs)
+    if outs is None:
+        outs = [(torch.empty((x.shape[0], x.shape[1] // 2), dtype=torch.uint8, device=dev),
+                 torch.empty((x.shape[0], x.shape[1] // block), dtype=torch.uint8, device=dev),
+                 torch.empty(1, dtype=torch.float32, device=dev)) for x in xs]
+    arr = (NVFP4Tensor * len(xs))()
+    for k, (x, w, (q, sc, S)) in enumerate(zip(xs, weights, outs)):
+        if x.dim() != 2 or not x.is_cuda or not x.is_contiguous() or x.dtype != xs[0].dtype:
+            raise ValueError("every tensor must be a contiguous 2-D device tensor of one dtype")
+        arr[k] = NVFP4Tensor(x.data_ptr(), x.shape[0], x.shape[1],
+                             None if w is None else w.data_ptr(), S.data_ptr(), q.data_ptr(),
+                             sc.data_ptr())
+    nbytes = nvfp4_batched_workspace_bytes(len(xs))
+    if ws is None or ws.numel() * ws.element_size() < nbytes:
+        ws = torch.empty(nbytes // 4, dtype=torch.int32, device=dev)
+    main = torch.cuda.current_stream(dev)
+    side = side_stream(dev) if overlap else main
+    if side is not main:
+        ws.record_stream(side)          # the reductions on the side stream write it
+    rc = nvfp4_quant_batched(METHOD_IDS[method], ctypes.cast(arr, ctypes.c_void_p), len(xs), dt,
+                             block, ctypes.c_float(D), _ptr(ws), nbytes,
+                             ctypes.c_void_p(main.cuda_stream), ctypes.c_void_p(side.cuda_stream))
+    if rc != 0:
+        raise NVFP4Error(rc, "nvfp4_quant_batched")
+    return outs
 
 
 def dequant(q: torch.Tensor, scales: torch.Tensor, S: torch.Tensor, block: int = 16,

@@ -112,3 +112,24 @@ def test_no_oracle_in_the_product_path():
     for f in list(pkg.rglob("*.py")) + list(pkg.rglob("*.hip")) + list(pkg.rglob("*.cpp")):
         text = f.read_text()
         assert "oracle" not in text.lower().replace("# the checker", ""), f
+
+
+def test_batched_validation(nv):
+    T = nv.nvfp4.NVFP4Tensor
+    arr = (T * 2)(T(0x100000, 4, 64, 0x100000, 0x100000, 0x100000, 0x100000),
+                  T(0x100000, 4, 64, 0x100000, 0x100000, 0x100000, 0x100000))
+    f = nv.nvfp4_quant_batched
+    ws, wsb = FAKE, nv.nvfp4_batched_workspace_bytes(2)
+    a = ctypes.cast(arr, ctypes.c_void_p)
+    assert f(3, a, -1, 1, 16, ctypes.c_float(256.0), ws, wsb, None, None) == -5
+    assert f(9, a, 2, 1, 16, ctypes.c_float(256.0), ws, wsb, None, None) == -5
+    assert f(3, None, 2, 1, 16, ctypes.c_float(256.0), ws, wsb, None, None) == -1
+    assert f(3, a, 2, 1, 16, ctypes.c_float(256.0), ws, wsb - 16, None, None) == -6
+    assert f(3, a, 2, 1, 24, ctypes.c_float(256.0), ws, wsb, None, None) == -3
+    assert f(3, a, 2, 7, 16, ctypes.c_float(256.0), ws, wsb, None, None) == -4
+    arr[1].cols = 60
+    assert f(3, a, 2, 1, 16, ctypes.c_float(256.0), ws, wsb, None, None) == -2
+    arr[1].cols = 64
+    arr[1].col_weight = None
+    assert f(3, a, 2, 1, 16, ctypes.c_float(256.0), ws, wsb, None, None) == -1
+    assert f(3, a, 0, 1, 16, ctypes.c_float(256.0), None, 0, None, None) == 0

@@ -257,3 +257,49 @@ def test_parity_online_sampled(nv):
         check(nv, "scalesweep_mse", x, 16, rows_sample=rows)
         check(nv, "scalesweep_mse", x, 16, static=0.01, rows_sample=rows)
         check(nv, "absmax", x, 16, rows_sample=rows)
+
+
+# ---------------------------------------------------------------------------------------
+# Batched call: the same outputs as the single-tensor calls, reductions overlapped on a side
+# stream.
+# ---------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("method", METHODS)
+@pytest.mark.parametrize("overlap", [True, False])
+def test_batched_matches_single_calls(nv, method, overlap):
+    g = workloads.generator(DEV, 8, 8)
+    shapes = [(512, 1024), (0, 64), (64, 4096), (1024, 512), (8, 64)]
+    xs = [workloads.llm_weight(r, c, g, DEV) if r else torch.zeros(0, c, device=DEV,
+          dtype=torch.bfloat16) for r, c in shapes]
+    ws = [workloads.column_importance(c, g, DEV, tokens=64) for _, c in shapes]
+    use_w = method in ("scalesweep_wmse", "four_over_six")
+    outs = nv.quantize_batched(xs, method, 16, weights=ws if use_w else None, overlap=overlap)
+    for k, x in enumerate(xs):
+        q1, sc1, S1 = nv.quantize(x, method, 16, weight=ws[k] if use_w else None)
+        torch.cuda.synchronize()
+        q2, sc2, S2 = outs[k]
+        assert torch.equal(S1, S2) and torch.equal(sc1, sc2) and torch.equal(q1, q2), (k, shapes[k])
+    # one tensor against the oracle as well
+    check_x, check_w = xs[2], ws[2].cpu().numpy() if use_w else None
+    S_ref, q_ref, sc_ref = oracle.quantize(method, workloads.host_array(check_x), 16,
+                                           RANGE[method], 0.0, check_w)
+    assert outs[2][2].item() == S_ref
+    assert np.array_equal(outs[2][1].cpu().numpy(), sc_ref)
+    assert np.array_equal(outs[2][0].cpu().numpy(), q_ref)
+
+
+def test_batched_full_layer_sampled(nv):
+    layer = workloads.llama8b_layer(DEV)
+    xs = [layer[n][0] for n in layer]
+    ws = [layer[n][1] for n in layer]
+    outs = nv.quantize_batched(xs, "scalesweep_wmse", 16, weights=ws)
+    torch.cuda.synchronize()
+    for i, (x, w, (q, sc, S)) in enumerate(zip(xs, ws, outs)):
+        rows = _sample_rows(x.shape[0], 16, 200 + i)
+        xh = workloads.host_array(x)
+        S_ref = oracle.tensor_scale(xh, 256.0)
+        assert S.item() == S_ref
+        _, q_ref, sc_ref = oracle.quantize("scalesweep_wmse", xh[rows], 16, 256.0, S_ref,
+                                           w.cpu().numpy())
+        assert np.array_equal(sc[rows].cpu().numpy(), sc_ref)
+        assert np.array_equal(q[rows].cpu().numpy(), q_ref)
