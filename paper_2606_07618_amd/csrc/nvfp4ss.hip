@@ -79,46 +79,65 @@ struct Scale {
     float M, rM, s, cvs;
 };
 
-// RN32(1 / (1 + b/8)) for a 3-bit significand b (the compiler folds each quotient with IEEE
-// division; a select chain keeps the table fill free of memory loads).
-__device__ __forceinline__ float recip_significand(uint32_t b) {
-    float r = 1.0f / 1.875f;
-    r = b == 6u ? 1.0f / 1.75f : r;
-    r = b == 5u ? 1.0f / 1.625f : r;
-    r = b == 4u ? 1.0f / 1.5f : r;
-    r = b == 3u ? 1.0f / 1.375f : r;
-    r = b == 2u ? 1.0f / 1.25f : r;
-    r = b == 1u ? 1.0f / 1.125f : r;
-    return b == 0u ? 1.0f : r;
-}
-
 // The table covers codes -16..143 so that a window's candidates index it without clamping.
 // Codes that are not candidates get NaN in M, rM and cvs, so their loss comes out NaN and
 // loses every comparison: codes outside 0..126, and code 0 unless the zero scale is allowed
 // (AbsMax and 4/6 may pick it; a ScaleSweep window starts at code 1).
 constexpr int kTabLo = 16, kTabSize = 160;
 
-// Fills the table (threads 0..159 write entry threadIdx.x - 16); the caller synchronizes
-// before reading it.
+struct ScaleTable {
+    Scale e[kTabSize];
+};
+
+constexpr float pow2(int k) {
+    float r = 1.0f;
+    for (; k > 0; --k) r *= 2.0f;
+    for (; k < 0; ++k) r *= 0.5f;
+    return r;
+}
+
+// Built at compile time (all steps exact except 1/M, which constant folding rounds to
+// nearest even): E4M3 code c = a*8 + b has value 2^(a-7) (1 + b/8) for a > 0 and
+// 2^-6 (b/8) for a = 0 (Appendix A with e = 4, m = 3).
 template <bool ZERO_SCALE>
-__device__ __forceinline__ void fill_scale_table(Scale* tab) {
-    const int c = (int)threadIdx.x - kTabLo;
-    if (c < kTabSize - kTabLo) {
-        const float nan = __uint_as_float(0x7FC00000u);
-        Scale e;
-        if (c < 0 || c > 126) {
-            e.M = e.rM = e.s = e.cvs = nan;
-        } else {
-            const float s = e4m3_value(c);
-            const uint32_t b = (__float_as_uint(s) >> 20) & 7u;   // s = (1 + b/8) 2^E exactly
-            const bool zero = c == 0;
-            e.M = zero ? (ZERO_SCALE ? 0.f : nan) : __uint_as_float((b << 20) | 0x3F800000u);
-            e.rM = zero ? (ZERO_SCALE ? 0.f : nan) : recip_significand(b);
+constexpr ScaleTable make_scale_table() {
+    ScaleTable t{};
+    const float nan = __builtin_nanf("");
+    for (int i = 0; i < kTabSize; ++i) {
+        const int c = i - kTabLo;
+        Scale e{nan, nan, nan, nan};
+        if (c >= 0 && c <= 126) {
+            const int a = c >> 3, b = c & 7;
+            const float s = a ? pow2(a - 7) * (1.0f + (float)b / 8.0f) : pow2(-6) * ((float)b / 8.0f);
             e.s = s;
-            e.cvs = zero ? (ZERO_SCALE ? 1.0f : nan) : s;
+            if (c == 0) {
+                if (ZERO_SCALE) {
+                    e.M = 0.0f;
+                    e.rM = 0.0f;
+                    e.cvs = 1.0f;
+                }
+            } else {
+                float M = s;                       // significand of s in [1, 2)
+                while (M >= 2.0f) M *= 0.5f;
+                while (M < 1.0f) M *= 2.0f;
+                e.M = M;
+                e.rM = 1.0f / M;
+                e.cvs = s;
+            }
         }
-        tab[c] = e;
+        t.e[i] = e;
     }
+    return t;
+}
+
+__device__ constexpr ScaleTable kSweepTable = make_scale_table<false>();
+__device__ constexpr ScaleTable kNearestTable = make_scale_table<true>();
+
+// Copies the table into LDS (threads 0..159); the caller synchronizes before reading it.
+template <bool ZERO_SCALE>
+__device__ __forceinline__ void fill_scale_table(Scale* tab_all) {
+    if (threadIdx.x < kTabSize)
+        tab_all[threadIdx.x] = (ZERO_SCALE ? kNearestTable : kSweepTable).e[threadIdx.x];
 }
 
 __device__ __forceinline__ int clamp_code(int c) { return c < 0 ? 0 : (c > 126 ? 126 : c); }
@@ -274,14 +293,18 @@ __device__ double exact_loss(const float (&y)[kLaneElems], const float (&w)[kLan
         if (part == l) {
 #pragma unroll
             for (int i = 0; i < kLaneElems; ++i) {
-                const float a = fabsf(y[i]);
+                float a = fabsf(y[i]);
+                float wi = w[i];
+                // keeps the binary64 conversions of |y| and w inside this rarely taken path
+                // (hoisted out of the candidate loop they would hold 64 registers everywhere)
+                asm volatile("" : "+v"(a), "+v"(wi));
                 const float u = div_by_significand(a, sc.M, sc.rM);
                 const uint32_t p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, u, 0.f, sc.cvs, 0);
                 const float2v g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(p, sc.cvs, 0);
                 const float gs = g.x * sc.M;                       // exact
                 const double e = (double)a - (double)gs;
                 double t = e * e;
-                if (WEIGHTED) t = (double)w[i] * t;
+                if (WEIGHTED) t = (double)wi * t;
                 acc = acc + t;
             }
         }
@@ -419,7 +442,7 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
 #pragma unroll
         for (int i = 0; i < kLaneElems; ++i) w[i] = 1.0f;
     }
-    fill_scale_table<METHOD == kAbsMax || METHOD == kFourSix>(tab);
+    fill_scale_table<METHOD == kAbsMax || METHOD == kFourSix>(tab_all);
     __syncthreads();
     float S, rS;
     if (p.dynamic) {      // formed by scale_kernel, earlier on the same stream
@@ -445,7 +468,7 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
     }
     float ymax = 0.f;
 #pragma unroll
-    for (int i = 0; i < kLaneElems; ++i) ymax = fmaxf(ymax, fabsf(y[i]));
+    for (int i = 0; i < kLaneElems; i += 2) ymax = fmaxf(ymax, fmaxf(fabsf(y[i]), fabsf(y[i + 1])));
     ymax = group_max<LPB>(ymax);
 
     // ---- choose the block scale code ---------------------------------------------------
@@ -514,7 +537,12 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
         // ordering except between losses within 2^-16 of each other, which the band re-scores
         uint32_t best = 0xFFFFFFFFu;
 #pragma unroll
-        for (int d = 0; d < NC; ++d) best = min(best, (__float_as_uint(J[d]) & 0xFFFFFF80u) | (uint32_t)d);
+        for (int d = 0; d < NC; d += 2) {
+            const uint32_t k0 = (__float_as_uint(J[d]) & 0xFFFFFF80u) | (uint32_t)d;
+            const uint32_t k1 = d + 1 < NC ? (__float_as_uint(J[d + 1]) & 0xFFFFFF80u) | (uint32_t)(d + 1)
+                                           : 0xFFFFFFFFu;
+            best = min(best, min(k0, k1));
+        }
         int dstar = (int)(best & 0x7Fu);
         const float j1 = __uint_as_float(best & 0xFFFFFF80u);
         const float bound = fmaf(j1, kBand, j1) + kBandAbs;
