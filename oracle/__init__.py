@@ -77,6 +77,9 @@ def _bind(lib):
         "nvfp4_ref_window_upper": (I, []),
         "nvfp4_ref_block_sweep": (I, [P, P, I, I, I, P, P, P, P, P, P]),
         "nvfp4_ref_block_choose": (I, [I, P, P, I]),
+        "nvfp4_ref_window_tight": (I, [I, I, I, P, P]),
+        "nvfp4_ref_window_codes": (I, [I, I, I, I, I, I, P, P]),
+        "nvfp4_ref_quant_scalesweep_window": (I, [P, I, I64, I64, I, P, I, I, I, F, F, P, P, P]),
         "nvfp4_ref_tensor_scale": (I, [P, I, I64, F, P]),
         "nvfp4_ref_quantize": (I, [I, P, I, I64, I64, I, F, F, P, P, P, P]),
         "nvfp4_ref_dequant": (I, [P, P, F, I64, I64, I, P]),
@@ -178,6 +181,51 @@ def block_choose(method: str | int, y, w=None) -> int:
     y = _f32(y)
     w = _f32(w)
     return _load().nvfp4_ref_block_choose(m, _ptr(y), _ptr(w), y.size)
+
+
+WINDOW_MODES = {"offsets": 0, "tight": 1}
+
+
+def window_tight(method: str | int, n: int, b: int) -> tuple[int, int]:
+    """(lower, upper) offsets of the per-mantissa window for mantissa field b."""
+    m = METHODS[method] if isinstance(method, str) else method
+    lo, hi = ctypes.c_int(), ctypes.c_int()
+    rc = _load().nvfp4_ref_window_tight(m, n, b, ctypes.byref(lo), ctypes.byref(hi))
+    if rc:
+        raise OracleError(rc, "window_tight")
+    return lo.value, hi.value
+
+
+def window_codes(method: str | int, n: int, mode: str, lo_off: int, hi_off: int,
+                 c0: int) -> tuple[int, int]:
+    """The code range [lo, hi] a block with base code c0 sweeps under a window variant."""
+    m = METHODS[method] if isinstance(method, str) else method
+    lo, hi = ctypes.c_int(), ctypes.c_int()
+    rc = _load().nvfp4_ref_window_codes(m, n, WINDOW_MODES[mode], lo_off, hi_off, c0,
+                                        ctypes.byref(lo), ctypes.byref(hi))
+    if rc:
+        raise OracleError(rc, "window_codes")
+    return lo.value, hi.value
+
+
+def quantize_window(x, block: int = 16, weight=None, mode: str = "offsets", lo: int = -3,
+                    hi: int = 7, fp8_range: float = 256.0, static_scale: float = 0.0):
+    """ScaleSweep with a window variant (MSE objective if weight is None, else WMSE).
+    Returns (S, q, scales) like quantize()."""
+    x, dt = _tensor(x)
+    if x.ndim != 2:
+        raise ValueError("x must be 2-D [rows, cols]")
+    rows, cols = x.shape
+    w = _f32(weight)
+    q = np.zeros((rows, cols // 2), dtype=np.uint8)
+    sc = np.zeros((rows, max(cols // block, 0)), dtype=np.uint8)
+    S = ctypes.c_float()
+    rc = _load().nvfp4_ref_quant_scalesweep_window(
+        _ptr(x), dt, rows, cols, block, _ptr(w), WINDOW_MODES.get(mode, mode) if isinstance(mode, str) else mode,
+        lo, hi, float(fp8_range), float(static_scale), ctypes.byref(S), _ptr(q), _ptr(sc))
+    if rc:
+        raise OracleError(rc, "quantize_window")
+    return S.value, q, sc
 
 
 def continuous_opt(y, w=None) -> tuple[float, float]:

@@ -199,6 +199,18 @@ int nvfp4_ref_block_sweep(const float* y, const float* w, int n, int L, int U,
     return REF_OK;
 }
 
+/* Argmin of L over the codes lo..hi, the smallest code on a tie (reading). */
+static int argmin_codes(const float* y, const float* w, int n, int lo, int hi)
+{
+    int best = lo;
+    double jb = nvfp4_ref_block_loss(y, w, n, nvfp4_ref_e4m3(lo));
+    for (int c = lo + 1; c <= hi; ++c) {
+        double J = nvfp4_ref_block_loss(y, w, n, nvfp4_ref_e4m3(c));
+        if (J < jb) { best = c; jb = J; }
+    }
+    return best;
+}
+
 /* The scale code a method picks for one block of normalized values.
  *   AbsMax (NVFP4 section): s = round-to-nearest-FP8(max|y| / 6).
  *   4/6 (Introduction; Related Work): also try round-to-nearest-FP8(max|y| / 4), which maps the
@@ -222,13 +234,64 @@ int nvfp4_ref_block_choose(int method, const float* y, const float* w, int n)
     int lo = c0 - L < 1 ? 1 : c0 - L;
     int hi = c0 + U > E4M3_MAX_CODE ? E4M3_MAX_CODE : c0 + U;
     const float* wm = (method == REF_SCALESWEEP_WMSE) ? w : NULL;
-    int best = lo;
-    double jb = nvfp4_ref_block_loss(y, wm, n, nvfp4_ref_e4m3(lo));
-    for (int c = lo + 1; c <= hi; ++c) {
-        double J = nvfp4_ref_block_loss(y, wm, n, nvfp4_ref_e4m3(c));
-        if (J < jb) { best = c; jb = J; }
+    return argmin_codes(y, wm, n, lo, hi);
+}
+
+/* ------------------------------------------------------------------------------------- */
+/* Window variants (Block Scale Upper Bound / Lower Bound paragraphs; the sweep-range      */
+/* study of the Experiment section).                                                      */
+/* ------------------------------------------------------------------------------------- */
+
+/* Per-mantissa offsets for a base code whose mantissa field is b (Tables 1 and 2), derived
+ * on a normal base code (exponent field 7, s_base^FP8 = 1 + b/8) from the bounds' meaning:
+ *   upper: I of the largest round-down of (12/7) s_base, over s_base from s_base^FP8 up to the
+ *          next FP8 value (closed at the top, as the printed sup column is), minus I(s_base^FP8)
+ *          -- Lemma 1 with Lemma 2 at alpha = 12/7; it holds for either objective and any n;
+ *   lower: MSE objective with n = 16: I(s_base^FP8) minus I of the round-up of
+ *          (4/5) s_base^FP8 (Lemma 3); otherwise the method's standard lower offset. */
+int nvfp4_ref_window_tight(int method, int n, int b, int* lower, int* upper)
+{
+    if (!lower || !upper) return REF_ERR_NULL;
+    if (b < 0 || b > 7) return REF_ERR_ARG;
+    if (method != REF_SCALESWEEP_MSE && method != REF_SCALESWEEP_WMSE) return REF_ERR_ARG;
+    int std_lower = nvfp4_ref_window_lower(method, n);
+    if (std_lower < 0) return REF_ERR_BLOCK;
+    int c0 = 8 * 7 + b;
+    double s0 = nvfp4_ref_e4m3(c0);
+    double s1 = nvfp4_ref_e4m3(c0 + 1);
+    *upper = nvfp4_ref_floor_fp8(12.0 * s1, 7.0) - c0;
+    if (method == REF_SCALESWEEP_MSE && n == 16) {
+        int c_inf = c0;
+        while (c_inf > 1 && 5.0 * nvfp4_ref_e4m3(c_inf - 1) >= 4.0 * s0) --c_inf;
+        *lower = c0 - c_inf;
+    } else {
+        *lower = std_lower;
     }
-    return best;
+    return REF_OK;
+}
+
+/* The codes one block sweeps under a window variant, from its base code c0 = I(s_base^FP8):
+ *   mode REF_WINDOW_OFFSETS: offsets [lo_off, hi_off] around c0 (the [l, r] of the sweep-range
+ *     study; the standard windows are [-3, 7] and [-8, 7] at n = 16);
+ *   mode REF_WINDOW_TIGHT: the per-mantissa offsets of nvfp4_ref_window_tight for b = c0 & 7.
+ * reading: each end is clamped into the positive codes 1..126, so a window that lies wholly
+ * outside them sweeps the nearest end code alone; [-126, 126] is the exhaustive sweep. */
+int nvfp4_ref_window_codes(int method, int n, int mode, int lo_off, int hi_off, int c0,
+                           int* lo, int* hi)
+{
+    if (!lo || !hi) return REF_ERR_NULL;
+    if (mode == REF_WINDOW_TIGHT) {
+        int rc = nvfp4_ref_window_tight(method, n, c0 & 7, &lo_off, &hi_off);
+        if (rc != REF_OK) return rc;
+        lo_off = -lo_off;
+    } else if (mode != REF_WINDOW_OFFSETS || lo_off < -E4M3_MAX_CODE || hi_off > E4M3_MAX_CODE ||
+               lo_off > hi_off) {
+        return REF_ERR_ARG;
+    }
+    int l = c0 + lo_off, h = c0 + hi_off;
+    *lo = l < 1 ? 1 : l > E4M3_MAX_CODE ? E4M3_MAX_CODE : l;
+    *hi = h < 1 ? 1 : h > E4M3_MAX_CODE ? E4M3_MAX_CODE : h;
+    return REF_OK;
 }
 
 /* ------------------------------------------------------------------------------------- */
@@ -279,9 +342,12 @@ int nvfp4_ref_tensor_scale(const void* x, int dtype, int64_t count, float fp8_ra
     return REF_OK;
 }
 
-int nvfp4_ref_quantize(int method, const void* x, int dtype, int64_t rows, int64_t cols,
-                       int block, float fp8_range, float static_scale, const float* col_weight,
-                       float* tensor_scale, uint8_t* q, uint8_t* scales)
+/* win_mode < 0: the method's own block-scale rule; otherwise ScaleSweep over the window
+ * variant (win_mode, lo_off, hi_off) of nvfp4_ref_window_codes. */
+static int quantize_impl(int method, int win_mode, int lo_off, int hi_off, const void* x,
+                         int dtype, int64_t rows, int64_t cols, int block, float fp8_range,
+                         float static_scale, const float* col_weight, float* tensor_scale,
+                         uint8_t* q, uint8_t* scales)
 {
     if (method < REF_ABSMAX || method > REF_SCALESWEEP_WMSE) return REF_ERR_ARG;
     if (!tensor_scale) return REF_ERR_NULL;
@@ -291,6 +357,11 @@ int nvfp4_ref_quantize(int method, const void* x, int dtype, int64_t rows, int64
     if (!valid_range(fp8_range)) return REF_ERR_ARG;
     if (!isfinite(static_scale) || static_scale < 0.0f) return REF_ERR_ARG;
     if (method == REF_SCALESWEEP_WMSE && !col_weight) return REF_ERR_NULL;
+    if (win_mode >= 0) {
+        int lo, hi;
+        int rc = nvfp4_ref_window_codes(method, block, win_mode, lo_off, hi_off, 0, &lo, &hi);
+        if (rc != REF_OK) return rc;
+    }
     int64_t count = rows * cols;
     if (count > 0 && (!x || !q || !scales)) return REF_ERR_NULL;
     const float* w = (method == REF_SCALESWEEP_WMSE || method == REF_FOUR_OVER_SIX)
@@ -317,7 +388,15 @@ int nvfp4_ref_quantize(int method, const void* x, int dtype, int64_t rows, int64
                 if (!isfinite(v) || !isfinite(y[i])) return REF_ERR_NONFINITE;
             }
             const float* wb = w ? w + kb * block : NULL;
-            int c = nvfp4_ref_block_choose(method, y, wb, block);
+            int c;
+            if (win_mode < 0) {
+                c = nvfp4_ref_block_choose(method, y, wb, block);
+            } else {
+                int lo, hi;
+                int c0 = nvfp4_ref_floor_fp8(block_ymax(y, block), 6.0);
+                nvfp4_ref_window_codes(method, block, win_mode, lo_off, hi_off, c0, &lo, &hi);
+                c = argmin_codes(y, wb, block, lo, hi);
+            }
             scales[r * nb_row + kb] = (uint8_t)c;
             double s = nvfp4_ref_e4m3(c);
             for (int i = 0; i < block; ++i) {
@@ -334,6 +413,28 @@ int nvfp4_ref_quantize(int method, const void* x, int dtype, int64_t rows, int64
     }
     *tensor_scale = S;
     return REF_OK;
+}
+
+int nvfp4_ref_quantize(int method, const void* x, int dtype, int64_t rows, int64_t cols,
+                       int block, float fp8_range, float static_scale, const float* col_weight,
+                       float* tensor_scale, uint8_t* q, uint8_t* scales)
+{
+    return quantize_impl(method, -1, 0, 0, x, dtype, rows, cols, block, fp8_range,
+                         static_scale, col_weight, tensor_scale, q, scales);
+}
+
+/* ScaleSweep with a window variant; col_weight NULL selects the MSE objective, otherwise
+ * the WMSE objective with those per-column weights. */
+int nvfp4_ref_quant_scalesweep_window(const void* x, int dtype, int64_t rows, int64_t cols,
+                                      int block, const float* col_weight, int win_mode,
+                                      int lo_off, int hi_off, float fp8_range,
+                                      float static_scale, float* tensor_scale, uint8_t* q,
+                                      uint8_t* scales)
+{
+    if (win_mode != REF_WINDOW_OFFSETS && win_mode != REF_WINDOW_TIGHT) return REF_ERR_ARG;
+    int method = col_weight ? REF_SCALESWEEP_WMSE : REF_SCALESWEEP_MSE;
+    return quantize_impl(method, win_mode, lo_off, hi_off, x, dtype, rows, cols, block,
+                         fp8_range, static_scale, col_weight, tensor_scale, q, scales);
 }
 
 int nvfp4_ref_quant_absmax(const void* x, int dtype, int64_t rows, int64_t cols, int block,

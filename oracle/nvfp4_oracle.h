@@ -34,6 +34,7 @@ enum {
 };
 
 enum { REF_ABSMAX = 0, REF_FOUR_OVER_SIX = 1, REF_SCALESWEEP_MSE = 2, REF_SCALESWEEP_WMSE = 3 };
+enum { REF_WINDOW_OFFSETS = 0, REF_WINDOW_TIGHT = 1 };
 
 /* Number formats (Appendix A). */
 double nvfp4_ref_eemm_value(int e, int m, int code);
@@ -52,6 +53,11 @@ int nvfp4_ref_window_upper(void);
 int nvfp4_ref_block_sweep(const float* y, const float* w, int n, int L, int U,
                           int* c0, int* lo, int* hi, int* c_win, int* c_full, double* J127);
 int nvfp4_ref_block_choose(int method, const float* y, const float* w, int n);
+
+/* Window variants (Tables 1 and 2; the sweep-range study). */
+int nvfp4_ref_window_tight(int method, int n, int b, int* lower, int* upper);
+int nvfp4_ref_window_codes(int method, int n, int mode, int lo_off, int hi_off, int c0,
+                           int* lo, int* hi);
 
 /* Tensor-level calls. */
 int nvfp4_ref_tensor_scale(const void* x, int dtype, int64_t count, float fp8_range, float* S);
@@ -72,6 +78,11 @@ int nvfp4_ref_quant_scalesweep_wmse(const void* x, int dtype, int64_t rows, int6
                                     int block, float fp8_range, float static_scale,
                                     const float* col_weight, float* tensor_scale, uint8_t* q,
                                     uint8_t* scales);
+int nvfp4_ref_quant_scalesweep_window(const void* x, int dtype, int64_t rows, int64_t cols,
+                                      int block, const float* col_weight, int win_mode,
+                                      int lo_off, int hi_off, float fp8_range,
+                                      float static_scale, float* tensor_scale, uint8_t* q,
+                                      uint8_t* scales);
 int nvfp4_ref_dequant(const uint8_t* q, const uint8_t* scales, float tensor_scale,
                       int64_t rows, int64_t cols, int block, float* out);
 

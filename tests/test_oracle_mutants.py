@@ -46,6 +46,13 @@ MUTANTS = [
     ("window_not_clamped_to_1", "int lo = c0 - L < 1 ? 1 : c0 - L;\n    int hi = c0 + U > E4M3_MAX_CODE ? E4M3_MAX_CODE : c0 + U;\n    const float* wm",
      "int lo = c0 - L < 0 ? 0 : c0 - L;\n    int hi = c0 + U > E4M3_MAX_CODE ? E4M3_MAX_CODE : c0 + U;\n    const float* wm"),
     ("zero_tensor_scale", "        *S = 1.0f;\n        return REF_OK;", "        *S = 0.5f;\n        return REF_OK;"),
+    ("tight_lower_strict", "5.0 * nvfp4_ref_e4m3(c_inf - 1) >= 4.0 * s0",
+     "5.0 * nvfp4_ref_e4m3(c_inf - 1) > 4.0 * s0"),
+    ("tight_upper_from_s0", "*upper = nvfp4_ref_floor_fp8(12.0 * s1, 7.0) - c0;",
+     "*upper = nvfp4_ref_floor_fp8(12.0 * s0, 7.0) - c0;"),
+    ("window_clamp_to_0", "*lo = l < 1 ? 1 : l > E4M3_MAX_CODE", "*lo = l < 0 ? 0 : l > E4M3_MAX_CODE"),
+    ("window_offsets_mirrored", "int l = c0 + lo_off, h = c0 + hi_off;",
+     "int l = c0 - hi_off, h = c0 - lo_off;"),
 ]
 
 
@@ -62,6 +69,6 @@ def test_planted_mistake_is_caught(name, orig, planted, tmp_path):
     env = dict(os.environ, NVFP4_ORACLE_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         "-m", "not slow", "tests/test_oracle_pins.py",
-                        "tests/test_oracle_bruteforce.py"],
+                        "tests/test_oracle_bruteforce.py", "tests/test_oracle_windows.py"],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"planted mistake {name} was not caught:\n{r.stdout[-2000:]}"
