@@ -9,6 +9,8 @@
  *   nvfp4_quant_four_over_six   4/6 (Introduction and Related Work)
  *   nvfp4_quant_scalesweep_mse  ScaleSweep with the MSE objective (Method section)
  *   nvfp4_quant_scalesweep_wmse ScaleSweep with the WMSE objective (Method section)
+ * plus nvfp4_quant_scalesweep_window (ScaleSweep over other sweep windows: Tables 1 and 2,
+ * and the sweep-range study of the Experiment section)
  * and nvfp4_dequant computes x_hat.
  *
  * Common conventions
@@ -53,7 +55,7 @@ typedef enum {
     NVFP4_ERR_SHAPE = -2,     /* rows < 0, cols < 0, or cols % block != 0 */
     NVFP4_ERR_BLOCK = -3,     /* block not in {16, 32, 64, 128} */
     NVFP4_ERR_DTYPE = -4,     /* dtype / out_dtype not supported */
-    NVFP4_ERR_ARG = -5,       /* fp8_range or static_scale out of range */
+    NVFP4_ERR_ARG = -5,       /* fp8_range, static_scale or a window out of range */
     NVFP4_ERR_WORKSPACE = -6, /* dynamic scale requested without a large enough workspace */
     NVFP4_ERR_ALIGN = -7,     /* x, col_weight or workspace not 16-byte aligned, q not 8 */
     NVFP4_ERR_HIP = -8        /* a kernel launch failed */
@@ -122,6 +124,34 @@ int nvfp4_quant_scalesweep_wmse(const void* x, int dtype, int64_t rows, int64_t 
                                 const float* col_weight, float fp8_range, float static_scale,
                                 float* tensor_scale, uint8_t* q, uint8_t* scales,
                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* Window of nvfp4_quant_scalesweep_window. */
+typedef enum { NVFP4_WINDOW_OFFSETS = 0, NVFP4_WINDOW_TIGHT = 1 } nvfp4_window;
+
+/* ScaleSweep over a chosen window of E4M3 bit patterns around c0 = I(s0) (s0 the FP8 value
+ * just below max|y| / 6, as above).  A block sweeps the codes [lo, hi] and keeps the exact
+ * argmin of L, the smallest code on a tie, where
+ *   window_mode NVFP4_WINDOW_OFFSETS: lo = c0 + window_lo, hi = c0 + window_hi -- the [l, r]
+ *     bit-pattern bounds of the sweep-range study (Experiment section, Scale Sweep Range);
+ *     -126 <= window_lo <= window_hi <= 126 (else NVFP4_ERR_ARG).  [-3, 7] is
+ *     nvfp4_quant_scalesweep_mse at block 16, [-8, 7] nvfp4_quant_scalesweep_wmse, and
+ *     [-126, 126] the exhaustive sweep over all 126 positive scales;
+ *   window_mode NVFP4_WINDOW_TIGHT: per-mantissa offsets for the mantissa field b = c0 & 7
+ *     (window_lo / window_hi ignored): hi = c0 + 7, or c0 + 6 for b = 6, 7 (Table 1, from
+ *     Lemmas 1 and 2; any objective and block); lo = c0 - 3 for b = 0, 7 and c0 - 2 otherwise
+ *     (Table 2, from Lemma 3) with the MSE objective at block 16, else the standard lower
+ *     offset of the objective.  Where the lemmas hold (normal s0 with 11/7 s0 <= 448) it
+ *     picks the same codes as the standard windows with 9 to 11 candidates instead of 11.
+ * Each end is clamped into 1..126, so a window wholly outside them sweeps that end code alone.
+ * col_weight NULL selects the MSE objective, otherwise the WMSE objective with those
+ * per-column weights (as nvfp4_quant_scalesweep_wmse).  Other arguments, layouts and errors
+ * as nvfp4_quant_scalesweep_wmse. */
+int nvfp4_quant_scalesweep_window(const void* x, int dtype, int64_t rows, int64_t cols,
+                                  int block, const float* col_weight, int window_mode,
+                                  int window_lo, int window_hi, float fp8_range,
+                                  float static_scale, float* tensor_scale, uint8_t* q,
+                                  uint8_t* scales, void* workspace, size_t workspace_bytes,
+                                  void* stream);
 
 /* One tensor of a batched call: device pointers and shape, as in the single-tensor calls
  * (col_weight: NULL unless the method uses weights). */

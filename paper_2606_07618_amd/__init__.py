@@ -17,9 +17,11 @@ from .nvfp4 import (  # noqa: F401
     nvfp4_quant_four_over_six,
     nvfp4_quant_scalesweep_mse,
     nvfp4_quant_scalesweep_wmse,
+    nvfp4_quant_scalesweep_window,
     nvfp4_status_string,
     nvfp4_workspace_bytes,
     quantize,
     quantize_batched,
+    quantize_window,
     workspace,
 )

@@ -46,7 +46,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kLaneElems = 16;
 
-enum Method { kAbsMax = 0, kFourSix = 1, kSweepMse = 2, kSweepWmse = 3 };
+enum Method { kAbsMax = 0, kFourSix = 1, kSweepMse = 2, kSweepWmse = 3, kWindowMse = 4, kWindowWmse = 5 };
 
 // Workspace words: one |x|-maximum bit pattern per workgroup of the reduction pass, then S
 // and 1/S.
@@ -395,6 +395,8 @@ struct Params {
     float S, rS;              // static global scale and its reciprocal
     const uint32_t* ws;       // workspace of the dynamic path
     float* tensor_scale;      // static path: written once, by the first lane of the grid
+    int win_tight;            // window variants: per-mantissa offsets (else win_lo..win_hi)
+    int win_lo, win_hi;
 };
 
 __device__ __forceinline__ uint32_t div_bpr(uint32_t n, const Params& p) {
@@ -412,13 +414,89 @@ struct Window {
     static constexpr int NC = L + U + 1;
 };
 
+// Window variants of ScaleSweep (Tables 1 and 2; the sweep-range study of the Experiment
+// section): the block sweeps the codes [lo, hi] = [c0 + lo_off, c0 + hi_off], each end clamped
+// into 1..126, with per-mantissa offsets in the tight mode:
+//   upper (Table 1, Lemmas 1-2 with alpha = 12/7, any objective and n): 7, or 6 for b >= 6;
+//   lower (Table 2, Lemma 3, MSE with n = 16): 3 for b = 0 and b = 7, else 2; otherwise the
+//   standard lower offset.
+// The window has 1..126 codes and may differ between the lanes of a wave, so the candidate
+// losses are not kept: a running minimum and second minimum of the keys decide the argmin and
+// whether the band re-scoring is needed, and that rare path scores the candidates again.
+template <bool WGT, int LPB>
+__device__ int choose_window(const float (&y)[kLaneElems], const float (&w)[kLaneElems], float ymax,
+                             const Scale* tab, const Params& p, int part, int group_base,
+                             int std_lower, bool table2) {
+    const int c0 = floor_code(ymax, 6.0f, 1.0f / 6.0f, tab);
+    int lo_off = p.win_lo, hi_off = p.win_hi;
+    if (p.win_tight) {
+        const int b = c0 & 7;
+        hi_off = b >= 6 ? 6 : 7;
+        lo_off = table2 ? ((b == 0 || b == 7) ? -3 : -2) : -std_lower;
+    }
+    const int lo = min(max(c0 + lo_off, 1), 126);
+    const int hi = min(max(c0 + hi_off, 1), 126);
+    const int ncand = hi - lo + 1;
+    uint32_t best1 = 0xFFFFFFFFu, best2 = 0xFFFFFFFFu;
+    auto take = [&](float J, int j) {
+        const uint32_t key = (__float_as_uint(J) & 0xFFFFFF80u) | (uint32_t)j;
+        best2 = min(best2, max(best1, key));
+        best1 = min(best1, key);
+    };
+    float u[kLaneElems];
+    if (__all(lo >= 8)) {
+        // normal codes only: lo + t, lo + t + 8, ... share the significand of lo + t
+        for (int t = 0; t < 8 && __any(t < ncand); ++t) {
+            const Scale st = tab[t < ncand ? lo + t : -kTabLo];        // -16: a NaN entry
+#pragma unroll
+            for (int i = 0; i < kLaneElems; ++i) u[i] = fabsf(y[i]) * st.rM;
+            for (int j = t; __any(j < ncand); j += 8) {
+                const Scale sj = tab[j < ncand ? lo + j : -kTabLo];
+                take(group_sum<LPB>(cand_loss<WGT>(u, y, w, sj.cvs, sj.M)), j);
+            }
+        }
+    } else {
+        for (int j = 0; __any(j < ncand); ++j) {
+            const Scale sj = tab[j < ncand ? lo + j : -kTabLo];
+#pragma unroll
+            for (int i = 0; i < kLaneElems; ++i) u[i] = fabsf(y[i]) * sj.rM;
+            take(group_sum<LPB>(cand_loss<WGT>(u, y, w, sj.cvs, sj.M)), j);
+        }
+    }
+    int dstar = (int)(best1 & 0x7Fu);
+    const float j1 = __uint_as_float(best1 & 0xFFFFFF80u);
+    const float bound = fmaf(j1, kBand, j1) + kBandAbs;
+    const bool near = __uint_as_float(best2 & 0xFFFFFF80u) <= bound;
+    if (__any(near)) {
+        if (near) {      // every lane of a block takes the same path (its losses are shared)
+            double jb = 0.0;
+            int db = -1;
+            for (int j = 0; j < ncand; ++j) {
+                const Scale sj = tab[lo + j];
+#pragma unroll
+                for (int i = 0; i < kLaneElems; ++i) u[i] = fabsf(y[i]) * sj.rM;
+                const float J = group_sum<LPB>(cand_loss<WGT>(u, y, w, sj.cvs, sj.M));
+                if (__uint_as_float(__float_as_uint(J) & 0xFFFFFF80u) <= bound) {
+                    const double jd = exact_loss<WGT, LPB>(y, w, sj, part, group_base);
+                    if (db < 0 || jd < jb) {
+                        jb = jd;
+                        db = j;
+                    }
+                }
+            }
+            if (db >= 0) dstar = db;
+        }
+    }
+    return dstar < ncand ? lo + dstar : lo;   // dstar >= ncand only if every loss is NaN
+}
+
 template <int METHOD, typename In, int N>
 __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ x,
                                                          const float* __restrict__ colw,
                                                          uint8_t* __restrict__ q,
                                                          uint8_t* __restrict__ scales, Params p) {
     constexpr int LPB = N / kLaneElems;
-    constexpr bool WEIGHTED_OBJ = METHOD == kSweepWmse || METHOD == kFourSix;
+    constexpr bool WEIGHTED_OBJ = METHOD == kSweepWmse || METHOD == kFourSix || METHOD == kWindowWmse;
     __shared__ Scale tab_all[kTabSize];
     Scale* tab = tab_all + kTabLo;                 // tab[c] for codes c in -16..143
     const int lane = threadIdx.x & 63;
@@ -501,6 +579,11 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
                 code = e4 < e6 ? c4 : c6;
             }
         }
+    } else if (METHOD == kWindowMse || METHOD == kWindowWmse) {
+        constexpr bool WGT = METHOD == kWindowWmse;
+        constexpr int STD_LOWER = Window<WGT ? kSweepWmse : kSweepMse, N>::L;
+        code = choose_window<WGT, LPB>(y, w, ymax, tab, p, part, group_base, STD_LOWER,
+                                        !WGT && N == 16);
     } else {
         using Win = Window<METHOD, N>;
         constexpr int NC = Win::NC;
@@ -670,6 +753,7 @@ struct Call {
     void* ws;
     size_t ws_bytes;
     hipStream_t stream;
+    int win_mode = 0, win_lo = 0, win_hi = 0;     // window variants only
 };
 
 template <int METHOD, typename In, int N>
@@ -706,7 +790,14 @@ int validate(const Call& c) {
     if (c.rows < 0 || c.cols < 0 || c.cols % c.block != 0) return NVFP4_ERR_SHAPE;
     if (!(c.fp8_range > 0.0f && c.fp8_range <= 448.0f)) return NVFP4_ERR_ARG;
     if (!(c.static_scale >= 0.0f && c.static_scale <= FLT_MAX)) return NVFP4_ERR_ARG;
-    if (c.method == kSweepWmse && !c.colw) return NVFP4_ERR_NULL;
+    if ((c.method == kSweepWmse || c.method == kWindowWmse) && !c.colw) return NVFP4_ERR_NULL;
+    if (c.method == kWindowMse || c.method == kWindowWmse) {
+        if (c.win_mode == NVFP4_WINDOW_OFFSETS) {
+            if (c.win_lo < -126 || c.win_hi > 126 || c.win_lo > c.win_hi) return NVFP4_ERR_ARG;
+        } else if (c.win_mode != NVFP4_WINDOW_TIGHT) {
+            return NVFP4_ERR_ARG;
+        }
+    }
     const int64_t n = c.rows * c.cols;
     if (n > 0 && (!c.x || !c.q || !c.scales)) return NVFP4_ERR_NULL;
     if (c.static_scale == 0.0f) {
@@ -753,12 +844,17 @@ hipError_t launch_main(const Call& c, hipStream_t stream) {
     p.rS = dynamic ? 0.0f : 1.0f / c.static_scale;
     p.ws = static_cast<const uint32_t*>(c.ws);
     p.tensor_scale = c.tensor_scale;
+    p.win_tight = c.win_mode == NVFP4_WINDOW_TIGHT ? 1 : 0;
+    p.win_lo = c.win_lo;
+    p.win_hi = c.win_hi;
     Call cs = c;
     cs.stream = stream;
     switch (c.method) {
         case kAbsMax: return launch_quant_m<kAbsMax>(cs, p);
         case kFourSix: return launch_quant_m<kFourSix>(cs, p);
         case kSweepMse: return launch_quant_m<kSweepMse>(cs, p);
+        case kWindowMse: return launch_quant_m<kWindowMse>(cs, p);
+        case kWindowWmse: return launch_quant_m<kWindowWmse>(cs, p);
         default: return launch_quant_m<kSweepWmse>(cs, p);
     }
 }
@@ -863,7 +959,7 @@ const char* nvfp4_status_string(int status) {
         case NVFP4_ERR_SHAPE: return "bad shape (rows/cols negative, cols not a multiple of block, or too many blocks)";
         case NVFP4_ERR_BLOCK: return "block must be 16, 32, 64 or 128";
         case NVFP4_ERR_DTYPE: return "unsupported dtype";
-        case NVFP4_ERR_ARG: return "fp8_range or static_scale out of range";
+        case NVFP4_ERR_ARG: return "fp8_range, static_scale or window out of range";
         case NVFP4_ERR_WORKSPACE: return "dynamic global scale needs a workspace of nvfp4_workspace_bytes() bytes";
         case NVFP4_ERR_ALIGN: return "misaligned pointer (x, col_weight, workspace: 16 bytes; q: 8 bytes)";
         case NVFP4_ERR_HIP: return "HIP kernel launch failed";
@@ -901,6 +997,21 @@ int nvfp4_quant_scalesweep_wmse(const void* x, int dtype, int64_t rows, int64_t 
     return run_quant({kSweepWmse, x, dtype, rows, cols, block, col_weight, fp8_range,
                       static_scale, tensor_scale, q, scales, workspace, workspace_bytes,
                       (hipStream_t)stream});
+}
+
+int nvfp4_quant_scalesweep_window(const void* x, int dtype, int64_t rows, int64_t cols,
+                                  int block, const float* col_weight, int window_mode,
+                                  int window_lo, int window_hi, float fp8_range,
+                                  float static_scale, float* tensor_scale, uint8_t* q,
+                                  uint8_t* scales, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+    Call c{col_weight ? kWindowWmse : kWindowMse, x, dtype, rows, cols, block, col_weight,
+           fp8_range, static_scale, tensor_scale, q, scales, workspace, workspace_bytes,
+           (hipStream_t)stream};
+    c.win_mode = window_mode;
+    c.win_lo = window_lo;
+    c.win_hi = window_hi;
+    return run_quant(c);
 }
 
 int nvfp4_dequant(const uint8_t* q, const uint8_t* scales, const float* tensor_scale,

@@ -42,6 +42,7 @@ def _load():
         "nvfp4_quant_four_over_six": (I, quant_w),
         "nvfp4_quant_scalesweep_mse": (I, quant),
         "nvfp4_quant_scalesweep_wmse": (I, quant_w),
+        "nvfp4_quant_scalesweep_window": (I, [P, I, I64, I64, I, P, I, I, I, F, F, P, P, P, P, SZ, P]),
         "nvfp4_dequant": (I, [P, P, P, I64, I64, I, I, P, P]),
     }
     for name, (res, args) in sigs.items():
@@ -67,6 +68,7 @@ nvfp4_quant_absmax = lib.nvfp4_quant_absmax
 nvfp4_quant_four_over_six = lib.nvfp4_quant_four_over_six
 nvfp4_quant_scalesweep_mse = lib.nvfp4_quant_scalesweep_mse
 nvfp4_quant_scalesweep_wmse = lib.nvfp4_quant_scalesweep_wmse
+nvfp4_quant_scalesweep_window = lib.nvfp4_quant_scalesweep_window
 nvfp4_dequant = lib.nvfp4_dequant
 nvfp4_batched_workspace_bytes = lib.nvfp4_batched_workspace_bytes
 nvfp4_quant_batched = lib.nvfp4_quant_batched
@@ -137,6 +139,53 @@ def quantize(x: torch.Tensor, method: str = "scalesweep_wmse", block: int = 16,
         raise ValueError(f"unknown method {method!r}")
     if rc != 0:
         raise NVFP4Error(rc, f"nvfp4_quant_{method}")
+    return q, sc, S
+
+
+WINDOW_MODES = {"offsets": 0, "tight": 1}
+
+
+def _check_input(x):
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D [rows, cols]")
+    if not x.is_cuda:
+        raise ValueError("x must be a device tensor (the library runs on the GPU only)")
+    if not x.is_contiguous():
+        raise ValueError("x must be contiguous")
+    if x.dtype == torch.bfloat16:
+        return BF16
+    if x.dtype == torch.float32:
+        return F32
+    raise TypeError("x must be bfloat16 or float32")
+
+
+def quantize_window(x: torch.Tensor, block: int = 16, weight: torch.Tensor | None = None,
+                    mode: str = "offsets", lo: int = -3, hi: int = 7,
+                    fp8_range: float = 256.0, static_scale: float = 0.0,
+                    ws: torch.Tensor | None = None, out=None):
+    """ScaleSweep over a window variant: ``mode`` "offsets" sweeps codes c0+lo .. c0+hi,
+    "tight" the per-mantissa windows; MSE objective if ``weight`` is None, else WMSE.
+    Returns (q, scales, S) like quantize()."""
+    dt = _check_input(x)
+    rows, cols = x.shape
+    if out is None:
+        q = torch.empty((rows, cols // 2), dtype=torch.uint8, device=x.device)
+        sc = torch.empty((rows, cols // block if block else 0), dtype=torch.uint8, device=x.device)
+        S = torch.empty(1, dtype=torch.float32, device=x.device)
+    else:
+        q, sc, S = out
+    if static_scale == 0.0 and ws is None:
+        ws = workspace(x.device)
+    wsb = 0 if ws is None else ws.numel() * ws.element_size()
+    if weight is not None and not (weight.is_cuda and weight.dtype == torch.float32
+                                   and weight.is_contiguous() and weight.numel() == cols):
+        raise ValueError("weight must be a contiguous float32 device tensor of length cols")
+    rc = nvfp4_quant_scalesweep_window(
+        _ptr(x), dt, rows, cols, block, _ptr(weight), WINDOW_MODES[mode], int(lo), int(hi),
+        ctypes.c_float(fp8_range), ctypes.c_float(static_scale), _ptr(S), _ptr(q), _ptr(sc),
+        _ptr(ws), wsb, _stream(x.device))
+    if rc != 0:
+        raise NVFP4Error(rc, "nvfp4_quant_scalesweep_window")
     return q, sc, S
 
 

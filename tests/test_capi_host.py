@@ -133,3 +133,23 @@ def test_batched_validation(nv):
     arr[1].col_weight = None
     assert f(3, a, 2, 1, 16, ctypes.c_float(256.0), ws, wsb, None, None) == -1
     assert f(3, a, 0, 1, 16, ctypes.c_float(256.0), None, 0, None, None) == 0
+
+
+def test_window_validation(nv):
+    f = nv.nvfp4_quant_scalesweep_window
+
+    def call(mode=0, lo=-3, hi=7, w=None, S=FAKE, block=16, static=1.0, cols=64):
+        return f(FAKE, 1, 4, cols, block, w, mode, lo, hi, ctypes.c_float(256.0),
+                 ctypes.c_float(static), S, FAKE, FAKE, None, 0, None)
+
+    assert call(mode=2) == -5
+    assert call(mode=-1) == -5
+    assert call(lo=2, hi=1) == -5
+    assert call(lo=-127) == -5
+    assert call(hi=127) == -5
+    assert call(S=None) == -1
+    assert call(block=24) == -3
+    assert call(cols=40) == -2
+    assert call(static=0.0) == -6              # dynamic scale without a workspace
+    assert call(w=P(0x100004)) == -7           # misaligned weights
+    assert call(mode=1, lo=99, hi=-99, static=-1.0) == -5
