@@ -190,6 +190,45 @@ int nvfp4_quant_batched(int method, const nvfp4_tensor* tensors, int count, int 
 int nvfp4_dequant(const uint8_t* q, const uint8_t* scales, const float* tensor_scale,
                   int64_t rows, int64_t cols, int block, int out_dtype, void* out, void* stream);
 
+/*
+ * Reference scales and exact losses for gap reports (appendix "Optimal FP32 Scale for FP4
+ * Quantization"; the relative gaps of Figures 1 and 4).  These are analysis calls, not
+ * quantizers.  Each works on y = RN32(x / S) with S read from the device float
+ * *tensor_scale (e.g. the one a quantizer call wrote), blocks and weights as in the
+ * quantizers (col_weight NULL: MSE objective).  Outputs are per micro-block, in block order
+ * (row-major over [rows, cols/block]); every value is computed in binary64 with a fixed
+ * order of correctly rounded operations.  x needs only its element alignment here.
+ */
+
+/* Optimal real block scale (appendix, first paragraph): opt_loss[b] = min over real s > 0 of
+ * L(s; y, w), found by enumerating the pieces between the breakpoints |y_i| / m_k
+ * (m_k the midpoints between neighbouring E2M1 values), on each of which L is a quadratic in
+ * s, and minimizing every piece on its closed interval; the lowest piece wins a tie, and the
+ * all-zero reconstruction (s -> infinity) wins a tie with any piece.  opt_scale[b] receives
+ * the minimizer (+infinity for the all-zero reconstruction, 1 for an all-zero block).
+ * FP8-quantized optimal scale (appendix, second paragraph): of the two E4M3 values just below
+ * and just above opt_scale[b] (codes >= 1), the one with the lower L, the lower one on a tie:
+ * fp8_code[b] its code and fp8_loss[b] its loss.  opt_loss [nblocks] is required (8-byte
+ * aligned); opt_scale, fp8_code and fp8_loss may be NULL.  One wavefront per block; binary64
+ * ALU-bound. */
+int nvfp4_block_optimum(const void* x, int dtype, int64_t rows, int64_t cols, int block,
+                        const float* col_weight, const float* tensor_scale, double* opt_loss,
+                        double* opt_scale, uint8_t* fp8_code, double* fp8_loss, void* stream);
+
+/* Exact loss L(E4M3(scales[b]); y, w) of every block at its given scale code (0..126; larger
+ * codes are read as 126), summed in element order in binary64: loss [nblocks], 8-byte
+ * aligned.  With the codes a quantizer chose, sum(loss) / sum(opt_loss) - 1 is its gap. */
+int nvfp4_block_loss(const void* x, int dtype, int64_t rows, int64_t cols, int block,
+                     const float* col_weight, const float* tensor_scale, const uint8_t* scales,
+                     double* loss, void* stream);
+
+/* Deterministic sum of v[0..n) in binary64 into the device double *out (a fixed reduction
+ * order that depends on n only).  workspace: >= nvfp4_sum_workspace_bytes() bytes, 8-byte
+ * aligned, no initialization. */
+size_t nvfp4_sum_workspace_bytes(void);
+int nvfp4_sum_f64(const double* v, int64_t n, double* out, void* workspace,
+                  size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -8,9 +8,14 @@ library is not built, importing the binding raises.
 from .nvfp4 import (  # noqa: F401
     LIB_PATH,
     NVFP4Error,
+    block_loss,
+    block_optimum,
     dequant,
+    gap_report,
     lib,
     nvfp4_batched_workspace_bytes,
+    nvfp4_block_loss,
+    nvfp4_block_optimum,
     nvfp4_dequant,
     nvfp4_quant_batched,
     nvfp4_quant_absmax,
@@ -19,9 +24,12 @@ from .nvfp4 import (  # noqa: F401
     nvfp4_quant_scalesweep_wmse,
     nvfp4_quant_scalesweep_window,
     nvfp4_status_string,
+    nvfp4_sum_f64,
+    nvfp4_sum_workspace_bytes,
     nvfp4_workspace_bytes,
     quantize,
     quantize_batched,
     quantize_window,
+    sum_f64,
     workspace,
 )

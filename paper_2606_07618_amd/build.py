@@ -8,6 +8,7 @@ from pathlib import Path
 HERE = Path(__file__).resolve().parent
 ROOT = HERE.parent
 SRC = HERE / "csrc" / "nvfp4ss.hip"
+SOURCES = [SRC, HERE / "csrc" / "optimum.hip"]
 LIB = HERE / "libnvfp4ss.so"
 
 HIPCC_FLAGS = [
@@ -20,7 +21,7 @@ HIPCC_FLAGS = [
 
 def build(out: Path = LIB, verbose: bool = False) -> Path:
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    cmd = [hipcc, *HIPCC_FLAGS, f"-I{ROOT / 'include'}", "-o", str(out), str(SRC)]
+    cmd = [hipcc, *HIPCC_FLAGS, f"-I{ROOT / 'include'}", "-o", str(out), *map(str, SOURCES)]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed:\n{r.stdout}\n{r.stderr}")

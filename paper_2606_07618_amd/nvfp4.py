@@ -44,6 +44,10 @@ def _load():
         "nvfp4_quant_scalesweep_wmse": (I, quant_w),
         "nvfp4_quant_scalesweep_window": (I, [P, I, I64, I64, I, P, I, I, I, F, F, P, P, P, P, SZ, P]),
         "nvfp4_dequant": (I, [P, P, P, I64, I64, I, I, P, P]),
+        "nvfp4_block_optimum": (I, [P, I, I64, I64, I, P, P, P, P, P, P, P]),
+        "nvfp4_block_loss": (I, [P, I, I64, I64, I, P, P, P, P, P]),
+        "nvfp4_sum_workspace_bytes": (SZ, []),
+        "nvfp4_sum_f64": (I, [P, I64, P, P, SZ, P]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(L, name)
@@ -70,6 +74,10 @@ nvfp4_quant_scalesweep_mse = lib.nvfp4_quant_scalesweep_mse
 nvfp4_quant_scalesweep_wmse = lib.nvfp4_quant_scalesweep_wmse
 nvfp4_quant_scalesweep_window = lib.nvfp4_quant_scalesweep_window
 nvfp4_dequant = lib.nvfp4_dequant
+nvfp4_block_optimum = lib.nvfp4_block_optimum
+nvfp4_block_loss = lib.nvfp4_block_loss
+nvfp4_sum_workspace_bytes = lib.nvfp4_sum_workspace_bytes
+nvfp4_sum_f64 = lib.nvfp4_sum_f64
 nvfp4_batched_workspace_bytes = lib.nvfp4_batched_workspace_bytes
 nvfp4_quant_batched = lib.nvfp4_quant_batched
 METHOD_IDS = {"absmax": 0, "four_over_six": 1, "scalesweep_mse": 2, "scalesweep_wmse": 3}
@@ -248,3 +256,85 @@ def dequant(q: torch.Tensor, scales: torch.Tensor, S: torch.Tensor, block: int =
     if rc != 0:
         raise NVFP4Error(rc, "nvfp4_dequant")
     return out
+
+
+# ---- reference scales and gap reports ------------------------------------------------------
+
+def _check_scale(S, device):
+    if not (S.is_cuda and S.dtype == torch.float32 and S.numel() >= 1 and S.device == device):
+        raise ValueError("S must be a float32 device tensor on x's device")
+
+
+def block_optimum(x: torch.Tensor, S: torch.Tensor, block: int = 16,
+                  weight: torch.Tensor | None = None):
+    """Per-block optimal real scale and FP8-quantized optimum on y = RN32(x / S).
+    Returns (opt_loss f64, opt_scale f64, fp8_code u8, fp8_loss f64), each [rows, cols/block]."""
+    dt = _check_input(x)
+    _check_scale(S, x.device)
+    rows, cols = x.shape
+    shape = (rows, cols // block)
+    out = (torch.empty(shape, dtype=torch.float64, device=x.device),
+           torch.empty(shape, dtype=torch.float64, device=x.device),
+           torch.empty(shape, dtype=torch.uint8, device=x.device),
+           torch.empty(shape, dtype=torch.float64, device=x.device))
+    rc = nvfp4_block_optimum(_ptr(x), dt, rows, cols, block, _ptr(weight), _ptr(S),
+                             *map(_ptr, out), _stream(x.device))
+    if rc != 0:
+        raise NVFP4Error(rc, "nvfp4_block_optimum")
+    return out
+
+
+def block_loss(x: torch.Tensor, S: torch.Tensor, scales: torch.Tensor, block: int = 16,
+               weight: torch.Tensor | None = None) -> torch.Tensor:
+    """Exact binary64 loss of every block of y = RN32(x / S) at its E4M3 code in ``scales``."""
+    dt = _check_input(x)
+    _check_scale(S, x.device)
+    rows, cols = x.shape
+    if not (scales.is_cuda and scales.dtype == torch.uint8 and scales.is_contiguous()
+            and scales.numel() == rows * (cols // block)):
+        raise ValueError("scales must be a contiguous uint8 device tensor [rows, cols/block]")
+    loss = torch.empty((rows, cols // block), dtype=torch.float64, device=x.device)
+    rc = nvfp4_block_loss(_ptr(x), dt, rows, cols, block, _ptr(weight), _ptr(S), _ptr(scales),
+                          _ptr(loss), _stream(x.device))
+    if rc != 0:
+        raise NVFP4Error(rc, "nvfp4_block_loss")
+    return loss
+
+
+def sum_f64(v: torch.Tensor) -> torch.Tensor:
+    """Deterministic binary64 sum of a contiguous float64 device tensor, as a [1] tensor."""
+    if not (v.is_cuda and v.dtype == torch.float64 and v.is_contiguous()):
+        raise ValueError("v must be a contiguous float64 device tensor")
+    out = torch.empty(1, dtype=torch.float64, device=v.device)
+    ws = torch.empty(nvfp4_sum_workspace_bytes() // 8, dtype=torch.float64, device=v.device)
+    rc = nvfp4_sum_f64(_ptr(v), v.numel(), _ptr(out), _ptr(ws), nvfp4_sum_workspace_bytes(),
+                       _stream(v.device))
+    if rc != 0:
+        raise NVFP4Error(rc, "nvfp4_sum_f64")
+    return out
+
+
+def gap_report(x: torch.Tensor, block: int = 16, weight: torch.Tensor | None = None,
+               methods=("absmax", "four_over_six", "scalesweep_mse", "scalesweep_wmse")) -> dict:
+    """Relative gap of each block-scale rule to the optimal real block scale, as in the
+    paper's Figures 1 and 4: sum of S^2 L over the blocks of the rule, over the same sum for
+    the optimum, minus one.  The objective is WMSE if ``weight`` is given, else MSE; each
+    method runs with its own global scale (D = 448 for AbsMax, 256 otherwise), the optimum and
+    its FP8-quantized version with D = 256.  Also reports the exhaustive FP8 sweep."""
+    def total(loss, S):
+        return float(sum_f64(loss.reshape(-1)).item()) * float(S.item()) ** 2
+
+    q, sc, S = quantize_window(x, block, weight, "offsets", -126, 126)
+    opt_loss, _, fp8_code, fp8_loss = block_optimum(x, S, block, weight)
+    j_opt = total(opt_loss, S)
+    report = {"optimum": 0.0}
+    if j_opt > 0:
+        report["fp8_quantized_optimum"] = total(fp8_loss, S) / j_opt - 1.0
+        report["exhaustive_fp8_sweep"] = total(block_loss(x, S, sc, block, weight), S) / j_opt - 1.0
+        for m in methods:
+            w_m = weight if m in ("four_over_six", "scalesweep_wmse") else None
+            if m == "scalesweep_wmse" and weight is None:
+                continue
+            _, sc_m, S_m = quantize(x, m, block, weight=w_m)
+            report[m] = total(block_loss(x, S_m, sc_m, block, weight), S_m) / j_opt - 1.0
+    return report

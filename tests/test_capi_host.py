@@ -153,3 +153,25 @@ def test_window_validation(nv):
     assert call(static=0.0) == -6              # dynamic scale without a workspace
     assert call(w=P(0x100004)) == -7           # misaligned weights
     assert call(mode=1, lo=99, hi=-99, static=-1.0) == -5
+
+
+def test_analysis_call_validation(nv):
+    opt = nv.nvfp4_block_optimum
+    # (x, dtype, rows, cols, block, w, S, opt_loss, opt_scale, code, fp8_loss, stream)
+    assert opt(FAKE, 1, 4, 64, 16, None, None, FAKE8, None, None, None, None) == -1
+    assert opt(FAKE, 2, 4, 64, 16, None, FAKE, FAKE8, None, None, None, None) == -4
+    assert opt(FAKE, 1, 4, 64, 24, None, FAKE, FAKE8, None, None, None, None) == -3
+    assert opt(FAKE, 1, 4, 60, 16, None, FAKE, FAKE8, None, None, None, None) == -2
+    assert opt(FAKE, 1, 4, 64, 16, None, FAKE, None, None, None, None, None) == -1
+    assert opt(FAKE, 1, 4, 64, 16, None, FAKE, P(0x100004), None, None, None, None) == -7
+    assert opt(FAKE, 1, 0, 64, 16, None, FAKE, None, None, None, None, None) == 0   # empty
+    loss = nv.nvfp4_block_loss
+    assert loss(FAKE, 1, 4, 64, 16, None, FAKE, None, FAKE8, None) == -1
+    assert loss(FAKE, 1, 4, 64, 16, None, FAKE, FAKE, P(0x100004), None) == -7
+    assert loss(FAKE, 1, 4, 64, 16, P(0x100002), FAKE, FAKE, FAKE8, None) == -7
+    s = nv.nvfp4_sum_f64
+    wsb = nv.nvfp4_sum_workspace_bytes()
+    assert s(FAKE8, 10, None, FAKE8, wsb, None) == -1
+    assert s(FAKE8, -1, FAKE8, FAKE8, wsb, None) == -2
+    assert s(FAKE8, 10, FAKE8, FAKE8, wsb - 8, None) == -6
+    assert s(P(0x100004), 10, FAKE8, FAKE8, wsb, None) == -7
