@@ -80,6 +80,10 @@ def _bind(lib):
         "nvfp4_ref_window_tight": (I, [I, I, I, P, P]),
         "nvfp4_ref_window_codes": (I, [I, I, I, I, I, I, P, P]),
         "nvfp4_ref_quant_scalesweep_window": (I, [P, I, I64, I64, I, P, I, I, I, F, F, P, P, P]),
+        "nvfp4_ref_swizzled_offset": (I64, [I64, I64, I64]),
+        "nvfp4_ref_scales_bytes": (I64, [I64, I64, I, I]),
+        "nvfp4_ref_quant_online": (I, [I, P, I, I64, I64, I, P, I64, I64, F, I, P, P, P]),
+        "nvfp4_ref_channel_sq_norms": (I, [P, I, I64, I64, I64, I64, I64, I64, P]),
         "nvfp4_ref_tensor_scale": (I, [P, I, I64, F, P]),
         "nvfp4_ref_quantize": (I, [I, P, I, I64, I64, I, F, F, P, P, P, P]),
         "nvfp4_ref_dequant": (I, [P, P, F, I64, I64, I, P]),
@@ -323,3 +327,53 @@ def normalize(x, S: float) -> np.ndarray:
     """y = RN32(x / S), as the oracle forms it (numpy float32 division is IEEE)."""
     xf = bf16_to_f32(x) if np.asarray(x).dtype == np.uint16 else np.asarray(x, np.float32)
     return (xf / np.float32(S)).astype(np.float32)
+
+
+# --- online quantization ------------------------------------------------------------------
+
+SCALE_LAYOUTS = {"row_major": 0, "swizzled": 1}
+
+
+def swizzled_offset(m: int, k: int, k16: int) -> int:
+    return _load().nvfp4_ref_swizzled_offset(m, k, k16)
+
+
+def scales_bytes(rows: int, cols: int, block: int, layout: str) -> int:
+    return _load().nvfp4_ref_scales_bytes(rows, cols, block, SCALE_LAYOUTS[layout])
+
+
+def quantize_online(method: str | int, x, static_scale: float, block: int = 16,
+                    importance=None, imp_groups: int = 1, imp_group_rows: int = 1,
+                    layout: str = "row_major"):
+    """Static-scale quantization with per-group importance vectors [imp_groups, cols].
+    Returns (q [rows, cols/2], scales (1-D for the swizzled layout))."""
+    m = METHODS[method] if isinstance(method, str) else method
+    x, dt = _tensor(x)
+    rows, cols = x.shape
+    imp = _f32(importance)
+    nbytes = scales_bytes(rows, cols, block, layout)
+    if nbytes < 0:
+        raise OracleError(-5, "quantize_online")
+    q = np.zeros((rows, cols // 2), dtype=np.uint8)
+    sc = np.zeros(max(nbytes, 1), dtype=np.uint8)[:nbytes]
+    rc = _load().nvfp4_ref_quant_online(m, _ptr(x), dt, rows, cols, block, _ptr(imp),
+                                        imp_groups, imp_group_rows, float(static_scale),
+                                        SCALE_LAYOUTS[layout], None, _ptr(q), _ptr(sc))
+    if rc:
+        raise OracleError(rc, "quantize_online")
+    if layout == "row_major":
+        sc = sc.reshape(rows, cols // block)
+    return q, sc
+
+
+def channel_sq_norms(x, group_rows: int = 1, groups: int = 1, group_div: int = 1,
+                     rep_out: int = 1) -> np.ndarray:
+    """[groups / group_div * rep_out, cols] binary32 squared channel norms (see the C doc)."""
+    x, dt = _tensor(x)
+    rows, cols = x.shape
+    out = np.zeros((groups // group_div * rep_out, cols), dtype=np.float32)
+    rc = _load().nvfp4_ref_channel_sq_norms(_ptr(x), dt, rows, cols, group_rows, groups,
+                                            group_div, rep_out, _ptr(out))
+    if rc:
+        raise OracleError(rc, "channel_sq_norms")
+    return out

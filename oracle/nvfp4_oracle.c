@@ -437,6 +437,118 @@ int nvfp4_ref_quant_scalesweep_window(const void* x, int dtype, int64_t rows, in
                          fp8_range, static_scale, col_weight, tensor_scale, q, scales);
 }
 
+/* ------------------------------------------------------------------------------------- */
+/* Online quantization of activations, KV cache and queries (implementation details:     */
+/* static global scale; importance vectors of the WMSE section; the swizzled scale layout  */
+/* of the operator benchmark).                                                            */
+/* ------------------------------------------------------------------------------------- */
+
+/* Byte offset of the scale of row m, scale column k in the swizzled layout of a scale matrix
+ * with k16 columns: the matrix is padded to a multiple of 128 rows and 4 columns and stored
+ * as tiles of 128 rows x 4 columns, tile-row-major; inside a tile, row m of the tile sits at
+ * (m mod 32) * 16 + (m div 32) * 4 and column k at k mod 4.  reading: this is the layout of
+ * vLLM's NVFP4 operators, which the paper's operator benchmark uses. */
+int64_t nvfp4_ref_swizzled_offset(int64_t m, int64_t k, int64_t k16)
+{
+    int64_t kt = (k16 + 3) / 4;
+    int64_t tile = (m / 128) * kt + k / 4;
+    int64_t mm = m % 128;
+    return tile * 512 + (mm % 32) * 16 + (mm / 32) * 4 + k % 4;
+}
+
+int64_t nvfp4_ref_scales_bytes(int64_t rows, int64_t cols, int block, int layout)
+{
+    if (!valid_block(block) || rows < 0 || cols < 0 || cols % block != 0) return -1;
+    int64_t k16 = cols / block;
+    if (layout == REF_SCALES_ROW_MAJOR) return rows * k16;
+    if (layout == REF_SCALES_SWIZZLED && block == 16)
+        return ((rows + 127) / 128 * 128) * ((k16 + 3) / 4 * 4);
+    return -1;
+}
+
+/* Quantize with a given (static, calibrated) global scale, the importance vector of row r
+ * being importance[((r / imp_group_rows) mod imp_groups) * cols ...] (imp_groups = 1: one
+ * vector for every row, as for activations; K, V and Q as [batch * heads * tokens, head_dim]
+ * rows take imp_group_rows = tokens and imp_groups = heads).  Each row is quantized on its
+ * own with its vector, exactly as a one-row tensor with that column weight and the same S.
+ * Scales go row-major or swizzled (block 16 only; padding bytes are 0).  importance may be
+ * NULL for the unweighted methods; tensor_scale may be NULL. */
+int nvfp4_ref_quant_online(int method, const void* x, int dtype, int64_t rows, int64_t cols,
+                           int block, const float* importance, int64_t imp_groups,
+                           int64_t imp_group_rows, float static_scale, int layout,
+                           float* tensor_scale, uint8_t* q, uint8_t* scales)
+{
+    if (method < REF_ABSMAX || method > REF_SCALESWEEP_WMSE) return REF_ERR_ARG;
+    if (dtype != 0 && dtype != 1) return REF_ERR_DTYPE;
+    if (!valid_block(block)) return REF_ERR_BLOCK;
+    if (rows < 0 || cols < 0 || cols % block != 0) return REF_ERR_SHAPE;
+    if (!(static_scale > 0.0f) || !isfinite(static_scale)) return REF_ERR_ARG;
+    if (method == REF_SCALESWEEP_WMSE && !importance) return REF_ERR_NULL;
+    if (importance && (imp_groups < 1 || imp_group_rows < 1)) return REF_ERR_ARG;
+    int64_t nbytes = nvfp4_ref_scales_bytes(rows, cols, block, layout);
+    if (nbytes < 0) return REF_ERR_ARG;
+    if (rows * cols > 0 && (!x || !q || !scales)) return REF_ERR_NULL;
+    int64_t k16 = cols / block;
+    uint8_t* row_scales = k16 > 0 ? (uint8_t*)malloc((size_t)k16) : NULL;
+    if (k16 > 0 && !row_scales) return REF_ERR_ARG;
+    if (layout == REF_SCALES_SWIZZLED) memset(scales, 0, (size_t)nbytes);
+    size_t esz = dtype == 0 ? 4 : 2;
+    int rc = REF_OK;
+    for (int64_t r = 0; r < rows && rc == REF_OK; ++r) {
+        const float* w = importance
+                             ? importance + ((r / imp_group_rows) % imp_groups) * cols
+                             : NULL;
+        float S;
+        rc = nvfp4_ref_quantize(method, (const char*)x + (size_t)(r * cols) * esz, dtype, 1,
+                                cols, block, 448.0f, static_scale, w, &S, q + r * (cols / 2),
+                                row_scales);
+        for (int64_t k = 0; k < k16; ++k) {
+            int64_t off = layout == REF_SCALES_SWIZZLED ? nvfp4_ref_swizzled_offset(r, k, k16)
+                                                        : r * k16 + k;
+            scales[off] = row_scales[k];
+        }
+    }
+    free(row_scales);
+    if (rc == REF_OK && tensor_scale) *tensor_scale = static_scale;
+    return rc;
+}
+
+/* Squared norms of the input channels (the importance scores of the WMSE section): for a
+ * matrix x [rows, cols], out[g][c] = sum over the rows r of group g of x[r][c]^2, where row
+ * r belongs to group ((r / group_rows) mod groups) / group_div, summed in row order in
+ * binary64 and rounded once to binary32; each group's vector is written rep_out times
+ * (out has groups / group_div * rep_out vectors).  Activations: the weight matrix
+ * [d_out, d_in] with one group; queries from keys and keys from queries of grouped-query
+ * attention: rows [batch * heads * tokens, head_dim] with group_rows = tokens; values from
+ * W^O [d_model, heads * head_dim] viewed as [d_model * heads, head_dim] with group_rows = 1
+ * and groups = heads. */
+int nvfp4_ref_channel_sq_norms(const void* x, int dtype, int64_t rows, int64_t cols,
+                               int64_t group_rows, int64_t groups, int64_t group_div,
+                               int64_t rep_out, float* out)
+{
+    if (dtype != 0 && dtype != 1) return REF_ERR_DTYPE;
+    if (rows < 0 || cols < 0) return REF_ERR_SHAPE;
+    if (group_rows < 1 || groups < 1 || group_div < 1 || rep_out < 1 || groups % group_div)
+        return REF_ERR_ARG;
+    if (!out || (rows * cols > 0 && !x)) return REF_ERR_NULL;
+    int64_t gout = groups / group_div;
+    double* acc = (double*)calloc((size_t)(gout * cols > 0 ? gout * cols : 1), sizeof(double));
+    if (!acc) return REF_ERR_ARG;
+    for (int64_t r = 0; r < rows; ++r) {
+        int64_t g = ((r / group_rows) % groups) / group_div;
+        for (int64_t c = 0; c < cols; ++c) {
+            double v = (double)load_elem(x, dtype, r * cols + c);
+            acc[g * cols + c] += v * v;
+        }
+    }
+    for (int64_t g = 0; g < gout; ++g)
+        for (int64_t j = 0; j < rep_out; ++j)
+            for (int64_t c = 0; c < cols; ++c)
+                out[(g * rep_out + j) * cols + c] = (float)acc[g * cols + c];
+    free(acc);
+    return REF_OK;
+}
+
 int nvfp4_ref_quant_absmax(const void* x, int dtype, int64_t rows, int64_t cols, int block,
                            float fp8_range, float static_scale, float* tensor_scale,
                            uint8_t* q, uint8_t* scales)

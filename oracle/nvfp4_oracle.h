@@ -35,6 +35,7 @@ enum {
 
 enum { REF_ABSMAX = 0, REF_FOUR_OVER_SIX = 1, REF_SCALESWEEP_MSE = 2, REF_SCALESWEEP_WMSE = 3 };
 enum { REF_WINDOW_OFFSETS = 0, REF_WINDOW_TIGHT = 1 };
+enum { REF_SCALES_ROW_MAJOR = 0, REF_SCALES_SWIZZLED = 1 };
 
 /* Number formats (Appendix A). */
 double nvfp4_ref_eemm_value(int e, int m, int code);
@@ -83,6 +84,16 @@ int nvfp4_ref_quant_scalesweep_window(const void* x, int dtype, int64_t rows, in
                                       int lo_off, int hi_off, float fp8_range,
                                       float static_scale, float* tensor_scale, uint8_t* q,
                                       uint8_t* scales);
+/* Online quantization (implementation details; importance vectors of the WMSE section). */
+int64_t nvfp4_ref_swizzled_offset(int64_t m, int64_t k, int64_t k16);
+int64_t nvfp4_ref_scales_bytes(int64_t rows, int64_t cols, int block, int layout);
+int nvfp4_ref_quant_online(int method, const void* x, int dtype, int64_t rows, int64_t cols,
+                           int block, const float* importance, int64_t imp_groups,
+                           int64_t imp_group_rows, float static_scale, int layout,
+                           float* tensor_scale, uint8_t* q, uint8_t* scales);
+int nvfp4_ref_channel_sq_norms(const void* x, int dtype, int64_t rows, int64_t cols,
+                               int64_t group_rows, int64_t groups, int64_t group_div,
+                               int64_t rep_out, float* out);
 int nvfp4_ref_dequant(const uint8_t* q, const uint8_t* scales, float tensor_scale,
                       int64_t rows, int64_t cols, int block, float* out);
 

@@ -53,6 +53,15 @@ MUTANTS = [
     ("window_clamp_to_0", "*lo = l < 1 ? 1 : l > E4M3_MAX_CODE", "*lo = l < 0 ? 0 : l > E4M3_MAX_CODE"),
     ("window_offsets_mirrored", "int l = c0 + lo_off, h = c0 + hi_off;",
      "int l = c0 - hi_off, h = c0 - lo_off;"),
+    ("swizzle_row_split", "(mm % 32) * 16 + (mm / 32) * 4", "(mm / 4) * 16 + (mm % 4) * 4"),
+    ("norm_group_div_dropped", "int64_t g = ((r / group_rows) % groups) / group_div;",
+     "int64_t g = ((r / group_rows) % groups) % (groups / group_div);"),
+    ("online_group_index", "importance + ((r / imp_group_rows) % imp_groups) * cols",
+     "importance + (r % imp_groups) * cols"),
+    ("optimum_piece_at_low_end", "double s_ref = (seg == 0) ? 0.5 * hi : (seg == nb) ? 2.0 * lo : 0.5 * (lo + hi);",
+     "double s_ref = (seg == 0) ? 0.5 * hi : (seg == nb) ? 2.0 * lo : lo;"),
+    ("fp8_opt_ceil_not_taken", "if (nvfp4_ref_e4m3(cf) < s_opt && cf < E4M3_MAX_CODE) cc = cf + 1;",
+     "if (nvfp4_ref_e4m3(cf) < s_opt && cf < E4M3_MAX_CODE) cc = cf;"),
 ]
 
 
@@ -69,6 +78,7 @@ def test_planted_mistake_is_caught(name, orig, planted, tmp_path):
     env = dict(os.environ, NVFP4_ORACLE_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         "-m", "not slow", "tests/test_oracle_pins.py",
-                        "tests/test_oracle_bruteforce.py", "tests/test_oracle_windows.py"],
+                        "tests/test_oracle_bruteforce.py", "tests/test_oracle_windows.py",
+                        "tests/test_oracle_optimum.py", "tests/test_oracle_online.py"],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"planted mistake {name} was not caught:\n{r.stdout[-2000:]}"
