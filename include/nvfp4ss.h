@@ -153,6 +153,59 @@ int nvfp4_quant_scalesweep_window(const void* x, int dtype, int64_t rows, int64_
                                   uint8_t* scales, void* workspace, size_t workspace_bytes,
                                   void* stream);
 
+/*
+ * Online quantization of activations, KV cache and query states (implementation details:
+ * a static global scale found at calibration; importance vectors as in the WMSE section).
+ */
+typedef enum { NVFP4_SCALES_ROW_MAJOR = 0, NVFP4_SCALES_SWIZZLED = 1 } nvfp4_scale_layout;
+
+/* Bytes of the scale output of a [rows, cols] tensor: rows * cols / block row-major; for the
+ * swizzled layout (block 16 only) the scale matrix padded to multiples of 128 rows and 4
+ * columns.  A negative nvfp4_status for invalid arguments. */
+int64_t nvfp4_scales_bytes(int64_t rows, int64_t cols, int block, int layout);
+
+/* Quantizes x [rows, cols] with a given static global scale S = static_scale (finite, > 0,
+ * else NVFP4_ERR_ARG; every |x| / S must be finite) and method 0 AbsMax, 1 4/6,
+ * 2 ScaleSweep-MSE, 3 ScaleSweep-WMSE (same block-scale rules as the single-tensor calls).
+ * importance: [imp_groups, cols] binary32 (16-byte aligned, finite, >= 0), the weights of
+ * row r being vector ((r / imp_group_rows) mod imp_groups): one vector for activations
+ * [tokens, d_in] (imp_groups = 1), per head for K, V or Q laid out as
+ * [batch * heads * tokens, head_dim] (imp_groups = heads, imp_group_rows = tokens).  Required
+ * for method 3, optional for 4/6, ignored otherwise.  scale_layout NVFP4_SCALES_ROW_MAJOR
+ * writes scales [rows, cols/block]; NVFP4_SCALES_SWIZZLED (block 16) writes the 128 x 4 tiled
+ * layout of vLLM's NVFP4 GEMM operands -- byte
+ *   ((m / 128) * kt + k / 4) * 512 + (m mod 32) * 16 + ((m / 32) mod 4) * 4 + k mod 4
+ * for row m, scale column k, kt = ceil(cols / 64) -- and zeroes its padding; the buffer holds
+ * nvfp4_scales_bytes() bytes.  tensor_scale: NULL, or a device float that receives S.  No
+ * workspace, no reduction pass: one quantization kernel (plus a padding kernel for the
+ * swizzled layout), asynchronous on `stream`.  Other errors as the single-tensor calls. */
+int nvfp4_quant_online(int method, const void* x, int dtype, int64_t rows, int64_t cols, int block,
+                       const float* importance, int64_t imp_groups, int64_t imp_group_rows,
+                       float static_scale, int scale_layout, float* tensor_scale, uint8_t* q,
+                       uint8_t* scales, void* stream);
+
+/* Importance vectors (WMSE section): squared norms of input channels.  For x [rows, cols]
+ * (binary32 or bfloat16), out[g][c] = sum of x[r][c]^2 over the rows r of group
+ * g = ((r / group_rows) mod groups) / group_div, accumulated in binary64 and rounded once to
+ * binary32, each group's vector written rep_out times: out is
+ * [groups / group_div * rep_out, cols] binary32.  groups % group_div == 0 and
+ * groups / group_div <= 64, else NVFP4_ERR_ARG.  Uses:
+ *   activations of a linear layer: x = its weight [d_out, d_in], one group;
+ *   query states from keys (grouped-query attention, heads_q = rep * heads_kv): x = K as
+ *     [batch * heads_kv * tokens, head_dim], group_rows = tokens, groups = heads_kv,
+ *     rep_out = rep -- one vector per query head;
+ *   keys from queries: x = Q as [batch * heads_q * tokens, head_dim], group_rows = tokens,
+ *     groups = heads_q, group_div = rep;
+ *   values from W^O [d_model, heads_q * head_dim]: x = W^O viewed as
+ *     [d_model * heads_q, head_dim], group_rows = 1, groups = heads_q, group_div = rep.
+ * Deterministic (fixed summation order: column-wise over 256-row chunks, then over chunks).
+ * workspace: >= nvfp4_channel_sq_norms_workspace_bytes() bytes, 8-byte aligned. */
+int64_t nvfp4_channel_sq_norms_workspace_bytes(int64_t rows, int64_t cols, int64_t groups,
+                                               int64_t group_div);
+int nvfp4_channel_sq_norms(const void* x, int dtype, int64_t rows, int64_t cols, int64_t group_rows,
+                           int64_t groups, int64_t group_div, int64_t rep_out, float* out,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
 /* One tensor of a batched call: device pointers and shape, as in the single-tensor calls
  * (col_weight: NULL unless the method uses weights). */
 typedef struct {

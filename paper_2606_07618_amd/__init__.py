@@ -10,25 +10,31 @@ from .nvfp4 import (  # noqa: F401
     NVFP4Error,
     block_loss,
     block_optimum,
+    channel_sq_norms,
     dequant,
     gap_report,
     lib,
     nvfp4_batched_workspace_bytes,
     nvfp4_block_loss,
     nvfp4_block_optimum,
+    nvfp4_channel_sq_norms,
+    nvfp4_channel_sq_norms_workspace_bytes,
     nvfp4_dequant,
     nvfp4_quant_batched,
     nvfp4_quant_absmax,
     nvfp4_quant_four_over_six,
+    nvfp4_quant_online,
     nvfp4_quant_scalesweep_mse,
     nvfp4_quant_scalesweep_wmse,
     nvfp4_quant_scalesweep_window,
+    nvfp4_scales_bytes,
     nvfp4_status_string,
     nvfp4_sum_f64,
     nvfp4_sum_workspace_bytes,
     nvfp4_workspace_bytes,
     quantize,
     quantize_batched,
+    quantize_online,
     quantize_window,
     sum_f64,
     workspace,

@@ -8,7 +8,7 @@ from pathlib import Path
 HERE = Path(__file__).resolve().parent
 ROOT = HERE.parent
 SRC = HERE / "csrc" / "nvfp4ss.hip"
-SOURCES = [SRC, HERE / "csrc" / "optimum.hip"]
+SOURCES = [SRC, HERE / "csrc" / "optimum.hip", HERE / "csrc" / "importance.hip"]
 LIB = HERE / "libnvfp4ss.so"
 
 HIPCC_FLAGS = [

@@ -397,12 +397,35 @@ struct Params {
     float* tensor_scale;      // static path: written once, by the first lane of the grid
     int win_tight;            // window variants: per-mantissa offsets (else win_lo..win_hi)
     int win_lo, win_hi;
+    int swizzled;             // scales in 128 x 4 tiles (else row-major)
+    uint32_t sw_kt;           // 4-column scale tiles per tile row
+    uint32_t wgroups;         // importance vectors: row r uses ((r / wg_rows) mod wgroups)
+    uint32_t wgr_magic, wgr_shift, wgn_magic, wgn_shift;   // dividers by wg_rows, wgroups
 };
 
+// n / d for the invariant divisor d behind (magic, shift) (shift 0: d = 1).
+__device__ __forceinline__ uint32_t div_magic(uint32_t n, uint32_t magic, uint32_t shift) {
+    if (shift == 0) return n;
+    const uint32_t hi = __umulhi(n, magic);
+    return (hi + ((n - hi) >> 1)) >> (shift - 1);
+}
+
 __device__ __forceinline__ uint32_t div_bpr(uint32_t n, const Params& p) {
-    if (p.bpr_shift == 0) return n;                       // bpr == 1
-    const uint32_t hi = __umulhi(n, p.bpr_magic);
-    return (hi + ((n - hi) >> 1)) >> (p.bpr_shift - 1);
+    return div_magic(n, p.bpr_magic, p.bpr_shift);
+}
+
+// Index of the importance vector of a row: (row / wg_rows) mod wgroups.
+__device__ __forceinline__ uint32_t weight_group(uint32_t row, const Params& p) {
+    const uint32_t t = div_magic(row, p.wgr_magic, p.wgr_shift);
+    return t - div_magic(t, p.wgn_magic, p.wgn_shift) * p.wgroups;
+}
+
+// Byte offset of the scale of row m, scale column k in the swizzled layout: the scale matrix,
+// padded to multiples of 128 rows and 4 columns, is stored as 512-byte tiles of 128 x 4,
+// tile-row-major; inside a tile row m sits at (m mod 32) * 16 + ((m / 32) mod 4) * 4 and column
+// k at k mod 4 (the layout of vLLM's NVFP4 operators, used by the paper's operator benchmark).
+__device__ __forceinline__ uint32_t swizzled_offset(uint32_t m, uint32_t k, uint32_t kt) {
+    return ((m >> 7) * kt + (k >> 2)) * 512u + (m & 31u) * 16u + ((m >> 5) & 3u) * 4u + (k & 3u);
 }
 
 template <int METHOD, int N>
@@ -512,10 +535,15 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
     Loader<In>::load(x + blk_c * N + part * kLaneElems, y);
     float w[kLaneElems];
     const bool use_w = WEIGHTED_OBJ && colw != nullptr;
+    uint32_t row = 0, kb = 0;         // the block's row and block column
+    if (use_w || p.swizzled) {
+        row = div_bpr((uint32_t)blk_c, p);
+        kb = (uint32_t)blk_c - row * p.bpr;
+    }
     if (use_w) {
-        const uint32_t row = div_bpr((uint32_t)blk_c, p);
-        const uint32_t kb = (uint32_t)blk_c - row * p.bpr;
-        load_weights(colw + (int64_t)kb * N + part * kLaneElems, w);
+        const float* wrow = colw;
+        if (p.wgroups > 1) wrow += (int64_t)weight_group(row, p) * p.bpr * N;
+        load_weights(wrow + (int64_t)kb * N + part * kLaneElems, w);
     } else {
 #pragma unroll
         for (int i = 0; i < kLaneElems; ++i) w[i] = 1.0f;
@@ -529,7 +557,7 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
     } else {
         S = p.S;
         rS = p.rS;
-        if (blockIdx.x == 0 && threadIdx.x == 0) p.tensor_scale[0] = S;
+        if (blockIdx.x == 0 && threadIdx.x == 0 && p.tensor_scale) p.tensor_scale[0] = S;
     }
     const bool fast_div = S >= 0x1p-26f && S <= 0x1p26f;
 
@@ -678,9 +706,31 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
     if (active) {
         uint2* dst = reinterpret_cast<uint2*>(q + ((blk * N + part * kLaneElems) >> 1));
         *dst = make_uint2(packed[0], packed[1]);
-        if (part == 0) scales[blk] = (uint8_t)code;
+        if (part == 0) scales[p.swizzled ? (int64_t)swizzled_offset(row, kb, p.sw_kt) : blk] = (uint8_t)code;
     }
     }
+}
+
+// Zero bytes of the swizzled scale layout that no block owns: rows rows..mp-1 (all kp columns),
+// then columns k16..kp-1 of rows 0..rows-1.  Disjoint from the bytes the quantization kernel
+// writes, so the two may run in either order.
+__global__ __launch_bounds__(256) void swizzle_pad_kernel(uint8_t* __restrict__ scales, uint32_t rows,
+                                                          uint32_t k16, uint32_t mp, uint32_t kp) {
+    const uint32_t t = blockIdx.x * 256u + threadIdx.x;
+    const uint32_t n_rows = (mp - rows) * kp;
+    const uint32_t wcols = kp - k16;
+    uint32_t m, k;
+    if (t < n_rows) {
+        m = rows + t / kp;
+        k = t % kp;
+    } else if (t < n_rows + rows * wcols) {
+        const uint32_t u = t - n_rows;
+        m = u / wcols;
+        k = k16 + u % wcols;
+    } else {
+        return;
+    }
+    scales[swizzled_offset(m, k, kp / 4)] = 0;
 }
 
 // ---------------------------------------------------------------------------------------
@@ -754,6 +804,8 @@ struct Call {
     size_t ws_bytes;
     hipStream_t stream;
     int win_mode = 0, win_lo = 0, win_hi = 0;     // window variants only
+    int layout = NVFP4_SCALES_ROW_MAJOR;          // online calls only
+    int64_t wgroups = 1, wgroup_rows = 1;
 };
 
 template <int METHOD, typename In, int N>
@@ -844,6 +896,11 @@ hipError_t launch_main(const Call& c, hipStream_t stream) {
     p.rS = dynamic ? 0.0f : 1.0f / c.static_scale;
     p.ws = static_cast<const uint32_t*>(c.ws);
     p.tensor_scale = c.tensor_scale;
+    p.swizzled = c.layout == NVFP4_SCALES_SWIZZLED ? 1 : 0;
+    p.sw_kt = (uint32_t)((c.cols / c.block + 3) / 4);
+    p.wgroups = (uint32_t)c.wgroups;
+    make_divider((uint32_t)c.wgroup_rows, &p.wgr_magic, &p.wgr_shift);
+    make_divider((uint32_t)c.wgroups, &p.wgn_magic, &p.wgn_shift);
     p.win_tight = c.win_mode == NVFP4_WINDOW_TIGHT ? 1 : 0;
     p.win_lo = c.win_lo;
     p.win_hi = c.win_hi;
@@ -935,9 +992,71 @@ int run_batched(int method, const nvfp4_tensor* t, int count, int dtype, int blo
     return ok ? NVFP4_OK : NVFP4_ERR_HIP;
 }
 
+// Bytes of the scale output for a layout, or a negative status.
+int64_t scales_bytes(int64_t rows, int64_t cols, int block, int layout) {
+    if (!valid_block(block)) return NVFP4_ERR_BLOCK;
+    if (rows < 0 || cols < 0 || cols % block != 0) return NVFP4_ERR_SHAPE;
+    const int64_t k16 = cols / block;
+    if (layout == NVFP4_SCALES_ROW_MAJOR) return rows * k16;
+    if (layout != NVFP4_SCALES_SWIZZLED || block != 16) return NVFP4_ERR_ARG;
+    return (rows + 127) / 128 * 128 * ((k16 + 3) / 4 * 4);
+}
+
+int run_online(const Call& c) {
+    if (c.method < kAbsMax || c.method > kSweepWmse) return NVFP4_ERR_ARG;
+    if (c.dtype != NVFP4_IN_F32 && c.dtype != NVFP4_IN_BF16) return NVFP4_ERR_DTYPE;
+    const int64_t nbytes = scales_bytes(c.rows, c.cols, c.block, c.layout);
+    if (nbytes < 0) return (int)nbytes;
+    if (!(c.static_scale > 0.0f && c.static_scale <= FLT_MAX)) return NVFP4_ERR_ARG;
+    if (c.method == kSweepWmse && !c.colw) return NVFP4_ERR_NULL;
+    if (c.colw && (c.wgroups < 1 || c.wgroup_rows < 1 || c.wgroups > 0xFFFFFFFFLL ||
+                   c.wgroup_rows > 0xFFFFFFFFLL))
+        return NVFP4_ERR_ARG;
+    const int64_t n = c.rows * c.cols;
+    if (n > 0 && (!c.x || !c.q || !c.scales)) return NVFP4_ERR_NULL;
+    if (n > 0 && (!aligned(c.x, 16) || !aligned(c.q, 8))) return NVFP4_ERR_ALIGN;
+    if (c.colw && !aligned(c.colw, 16)) return NVFP4_ERR_ALIGN;
+    if (n / c.block > 0x7FFFFFFFLL || nbytes > 0x7FFFFFFFLL) return NVFP4_ERR_SHAPE;
+    if (n == 0) {
+        if (!c.tensor_scale) return NVFP4_OK;
+        return launch_empty(c, c.stream) == hipSuccess ? NVFP4_OK : NVFP4_ERR_HIP;
+    }
+    Call cc = c;
+    if (!c.colw) cc.wgroups = cc.wgroup_rows = 1;
+    if (launch_main(cc, c.stream) != hipSuccess) return NVFP4_ERR_HIP;
+    if (c.layout == NVFP4_SCALES_SWIZZLED) {
+        const uint32_t rows = (uint32_t)c.rows, k16 = (uint32_t)(c.cols / 16);
+        const uint32_t mp = (rows + 127) / 128 * 128, kp = (k16 + 3) / 4 * 4;
+        const uint64_t pad = (uint64_t)(mp - rows) * kp + (uint64_t)rows * (kp - k16);
+        if (pad > 0) {
+            hipLaunchKernelGGL(swizzle_pad_kernel, dim3((unsigned)((pad + 255) / 256)), dim3(256), 0,
+                               c.stream, c.scales, rows, k16, mp, kp);
+            if (hipGetLastError() != hipSuccess) return NVFP4_ERR_HIP;
+        }
+    }
+    return NVFP4_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+int64_t nvfp4_scales_bytes(int64_t rows, int64_t cols, int block, int layout) {
+    return scales_bytes(rows, cols, block, layout);
+}
+
+int nvfp4_quant_online(int method, const void* x, int dtype, int64_t rows, int64_t cols, int block,
+                       const float* importance, int64_t imp_groups, int64_t imp_group_rows,
+                       float static_scale, int scale_layout, float* tensor_scale, uint8_t* q,
+                       uint8_t* scales, void* stream) {
+    Call c{method, x, dtype, rows, cols, block,
+           (method == kSweepWmse || method == kFourSix) ? importance : nullptr, 448.0f,
+           static_scale, tensor_scale, q, scales, nullptr, 0, (hipStream_t)stream};
+    c.layout = scale_layout;
+    c.wgroups = imp_groups;
+    c.wgroup_rows = imp_group_rows;
+    return run_online(c);
+}
 
 size_t nvfp4_workspace_bytes(void) { return kWorkspaceBytes; }
 

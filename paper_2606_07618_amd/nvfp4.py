@@ -48,6 +48,10 @@ def _load():
         "nvfp4_block_loss": (I, [P, I, I64, I64, I, P, P, P, P, P]),
         "nvfp4_sum_workspace_bytes": (SZ, []),
         "nvfp4_sum_f64": (I, [P, I64, P, P, SZ, P]),
+        "nvfp4_scales_bytes": (I64, [I64, I64, I, I]),
+        "nvfp4_quant_online": (I, [I, P, I, I64, I64, I, P, I64, I64, F, I, P, P, P, P]),
+        "nvfp4_channel_sq_norms_workspace_bytes": (I64, [I64, I64, I64, I64]),
+        "nvfp4_channel_sq_norms": (I, [P, I, I64, I64, I64, I64, I64, I64, P, P, SZ, P]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(L, name)
@@ -78,6 +82,10 @@ nvfp4_block_optimum = lib.nvfp4_block_optimum
 nvfp4_block_loss = lib.nvfp4_block_loss
 nvfp4_sum_workspace_bytes = lib.nvfp4_sum_workspace_bytes
 nvfp4_sum_f64 = lib.nvfp4_sum_f64
+nvfp4_scales_bytes = lib.nvfp4_scales_bytes
+nvfp4_quant_online = lib.nvfp4_quant_online
+nvfp4_channel_sq_norms_workspace_bytes = lib.nvfp4_channel_sq_norms_workspace_bytes
+nvfp4_channel_sq_norms = lib.nvfp4_channel_sq_norms
 nvfp4_batched_workspace_bytes = lib.nvfp4_batched_workspace_bytes
 nvfp4_quant_batched = lib.nvfp4_quant_batched
 METHOD_IDS = {"absmax": 0, "four_over_six": 1, "scalesweep_mse": 2, "scalesweep_wmse": 3}
@@ -338,3 +346,56 @@ def gap_report(x: torch.Tensor, block: int = 16, weight: torch.Tensor | None = N
             _, sc_m, S_m = quantize(x, m, block, weight=w_m)
             report[m] = total(block_loss(x, S_m, sc_m, block, weight), S_m) / j_opt - 1.0
     return report
+
+
+# ---- online quantization (static global scale) ----------------------------------------------
+
+SCALE_LAYOUTS = {"row_major": 0, "swizzled": 1}
+
+
+def quantize_online(x: torch.Tensor, method: str, static_scale: float, block: int = 16,
+                    importance: torch.Tensor | None = None, imp_groups: int = 1,
+                    imp_group_rows: int = 1, layout: str = "row_major", out=None):
+    """Quantize with a calibrated static global scale; importance [imp_groups, cols] selects a
+    vector per row group (see nvfp4_quant_online).  Returns (q, scales): scales is
+    [rows, cols/block] row-major or the flat swizzled buffer."""
+    dt = _check_input(x)
+    rows, cols = x.shape
+    nbytes = nvfp4_scales_bytes(rows, cols, block, SCALE_LAYOUTS[layout])
+    if nbytes < 0:
+        raise NVFP4Error(int(nbytes), "nvfp4_scales_bytes")
+    if importance is not None and not (importance.is_cuda and importance.dtype == torch.float32
+                                       and importance.is_contiguous()
+                                       and importance.numel() == imp_groups * cols):
+        raise ValueError("importance must be a contiguous float32 device tensor [imp_groups, cols]")
+    if out is None:
+        q = torch.empty((rows, cols // 2), dtype=torch.uint8, device=x.device)
+        sc = torch.empty(nbytes, dtype=torch.uint8, device=x.device)
+    else:
+        q, sc = out
+    rc = nvfp4_quant_online(METHOD_IDS[method], _ptr(x), dt, rows, cols, block, _ptr(importance),
+                            imp_groups, imp_group_rows, ctypes.c_float(static_scale),
+                            SCALE_LAYOUTS[layout], None, _ptr(q), _ptr(sc), _stream(x.device))
+    if rc != 0:
+        raise NVFP4Error(rc, "nvfp4_quant_online")
+    if layout == "row_major" and out is None:
+        sc = sc.view(rows, cols // block)
+    return q, sc
+
+
+def channel_sq_norms(x: torch.Tensor, group_rows: int = 1, groups: int = 1, group_div: int = 1,
+                     rep_out: int = 1) -> torch.Tensor:
+    """Squared input-channel norms of x [rows, cols] per row group (importance vectors):
+    [groups / group_div * rep_out, cols] float32 (see nvfp4_channel_sq_norms)."""
+    dt = _check_input(x)
+    rows, cols = x.shape
+    need = nvfp4_channel_sq_norms_workspace_bytes(rows, cols, groups, group_div)
+    if need < 0:
+        raise NVFP4Error(int(need), "nvfp4_channel_sq_norms_workspace_bytes")
+    ws = torch.empty(max(need // 8, 1), dtype=torch.float64, device=x.device)
+    out = torch.empty((groups // group_div * rep_out, cols), dtype=torch.float32, device=x.device)
+    rc = nvfp4_channel_sq_norms(_ptr(x), dt, rows, cols, group_rows, groups, group_div, rep_out,
+                                _ptr(out), _ptr(ws), ws.numel() * 8, _stream(x.device))
+    if rc != 0:
+        raise NVFP4Error(rc, "nvfp4_channel_sq_norms")
+    return out

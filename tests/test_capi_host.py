@@ -175,3 +175,44 @@ def test_analysis_call_validation(nv):
     assert s(FAKE8, -1, FAKE8, FAKE8, wsb, None) == -2
     assert s(FAKE8, 10, FAKE8, FAKE8, wsb - 8, None) == -6
     assert s(P(0x100004), 10, FAKE8, FAKE8, wsb, None) == -7
+
+
+def test_online_validation(nv):
+    f = nv.nvfp4_quant_online
+
+    def call(method=2, dtype=1, rows=4, cols=64, block=16, imp=None, groups=1, grows=1,
+             S=1.0, layout=0, q=FAKE, sc=FAKE, x=FAKE):
+        return f(method, x, dtype, rows, cols, block, imp, groups, grows, ctypes.c_float(S),
+                 layout, None, q, sc, None)
+
+    assert call(method=4) == -5
+    assert call(S=0.0) == -5                     # the online path needs a static scale
+    assert call(S=float("inf")) == -5
+    assert call(layout=2) == -5
+    assert call(layout=1, block=32) == -5        # swizzled scales are for block 16
+    assert call(method=3) == -1                  # WMSE needs importance
+    assert call(method=3, imp=FAKE, groups=0) == -5
+    assert call(method=3, imp=FAKE, grows=0) == -5
+    assert call(method=3, imp=P(0x100004)) == -7
+    assert call(dtype=5) == -4
+    assert call(cols=40) == -2
+    assert call(q=None) == -1
+    assert call(x=P(0x100004)) == -7
+    assert nv.nvfp4_scales_bytes(130, 64, 16, 1) == 256 * 4
+    assert nv.nvfp4_scales_bytes(130, 64, 16, 0) == 130 * 4
+    assert nv.nvfp4_scales_bytes(4, 64, 32, 1) == -5
+    assert nv.nvfp4_scales_bytes(4, 60, 16, 0) == -2
+
+
+def test_channel_norms_validation(nv):
+    f = nv.nvfp4_channel_sq_norms
+    wsb = nv.nvfp4_channel_sq_norms_workspace_bytes(512, 64, 8, 2)
+    assert wsb == 2 * 4 * 64 * 8
+    assert nv.nvfp4_channel_sq_norms_workspace_bytes(512, 64, 3, 2) == -5
+    assert nv.nvfp4_channel_sq_norms_workspace_bytes(512, 64, 130, 2) == -5   # > 64 groups
+    assert f(FAKE, 3, 512, 64, 1, 8, 2, 1, FAKE, FAKE8, wsb, None) == -4
+    assert f(FAKE, 1, 512, 64, 0, 8, 2, 1, FAKE, FAKE8, wsb, None) == -5
+    assert f(FAKE, 1, 512, 64, 1, 8, 2, 0, FAKE, FAKE8, wsb, None) == -5
+    assert f(FAKE, 1, 512, 64, 1, 8, 2, 1, None, FAKE8, wsb, None) == -1
+    assert f(FAKE, 1, 512, 64, 1, 8, 2, 1, FAKE, FAKE8, wsb - 8, None) == -6
+    assert f(FAKE, 1, 512, 64, 1, 8, 2, 1, FAKE, P(0x100004), wsb, None) == -7
