@@ -10,7 +10,10 @@ per second (both objectives read the layer).  The line also carries:
     batched over the layer and as 7 single-tensor calls, and the time relative to AbsMax;
   * `roofline` for the dominant kernel (the WMSE sweep kernel), from HIP events around its
     launches on the stream it runs on;
-  * `cpu_baseline`: the oracle on the host, single-threaded, on a bounded sample.
+  * `cpu_baseline`: the oracle on the host, single-threaded, on a bounded sample;
+  * `rows`: the window variants, the reference scales (optimal real scale, FP8-quantized
+    optimum, gap report) and the online quantizer (static S, swizzled scales, importance
+    vectors), each timed on its own workload (skipped with --no-rows).
 Inputs are synthetic (workloads.py) and resident in HBM before timing starts.
 """
 from __future__ import annotations
@@ -47,6 +50,8 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain device copy of known size (for counter scaling)")
+    ap.add_argument("--no-rows", action="store_true",
+                    help="skip the window / reference-scale / online measurements")
     return ap.parse_args()
 
 
@@ -66,6 +71,75 @@ def read_traffic():
     if d.get("kernel_source_sha256_16", "").strip() != kernel_source_hash():
         return None
     return int(d["hbm_bytes_per_launch"])
+
+
+def _timed(torch, fn, reps):
+    """Mean milliseconds of fn over reps calls, HIP events on the current stream (which the
+    library launches on)."""
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def measure_rows(nv, workloads, torch, dev, layer):
+    """Window variants, reference scales and the online quantizer, each on its own
+    workload, as milliseconds per call and GB/s of bf16 input."""
+    out = {}
+    x, w = layer["gate_proj"]
+    n = x.numel()
+    S = 1.0e-4
+    win = {}
+    for name, wt, mode, lo, hi in (("tight_mse", None, "tight", 0, 0),
+                                   ("offsets_-3_7_mse", None, "offsets", -3, 7),
+                                   ("tight_wmse", w, "tight", 0, 0),
+                                   ("offsets_-8_7_wmse", w, "offsets", -8, 7),
+                                   ("exhaustive_mse", None, "offsets", -126, 126)):
+        ms = _timed(torch, lambda: nv.quantize_window(x, 16, wt, mode, lo, hi, 256.0, S),
+                    3 if name.startswith("exhaustive") else 10)
+        win[name] = {"ms": round(ms, 4), "input_GBps": round(2 * n / ms / 1e6, 1)}
+    out["f2_windows"] = {"workload": "gate_proj [14336, 4096] bf16, block 16, static S", **win}
+
+    xq, wq = layer["q_proj"]
+    _, _, Sq = nv.quantize(xq, "scalesweep_mse", 16)
+    ref = {}
+    for blk in (16, 128):
+        ms = _timed(torch, lambda: nv.block_optimum(xq, Sq, blk, wq), 2)
+        ref[f"block_optimum_n{blk}"] = {"ms": round(ms, 3),
+                                        "Gelem_per_s": round(xq.numel() / ms / 1e6, 3)}
+    gaps = nv.gap_report(xq, 16, wq)
+    out["f1_reference_scales"] = {"workload": "q_proj [4096, 4096] bf16, WMSE weights", **ref,
+                                  "gaps_wmse": {k: round(v, 5) for k, v in gaps.items()}}
+
+    t = workloads.online_tensors(dev)
+    onl = {}
+    for name in ("act", "k", "v", "q"):
+        xo = t[name].reshape(-1, t[name].shape[-1])
+        for m in ("absmax", "scalesweep_mse"):
+            ms = _timed(torch, lambda: nv.quantize_online(xo, m, 0.002, 16, layout="swizzled"), 10)
+            onl[f"{name}_{m}"] = {"shape": list(t[name].shape), "ms": round(ms, 4),
+                                  "input_GBps": round(2 * xo.numel() / ms / 1e6, 1)}
+    g = workloads.generator(dev, 77)
+    imp = workloads.column_importance(8192, g, dev, tokens=256)[None].contiguous()
+    table8 = {}
+    for B in (128, 1024, 8192, 32768):
+        xb = torch.randn((B, 8192), generator=g, device=dev).to(torch.bfloat16)
+        table8[str(B)] = {m: round(1e3 * _timed(torch, lambda: nv.quantize_online(
+            xb, m, 0.002, 16, imp, layout="swizzled"), 20), 1)
+            for m in ("absmax", "scalesweep_mse", "scalesweep_wmse")}
+    k2 = t["k"].reshape(-1, 128)
+    ms_imp = _timed(torch, lambda: nv.channel_sq_norms(k2, t["k"].shape[2], 8, 1, 4), 5)
+    out["f3_online"] = {"workload": "online tensors (activations [8192, 4096]; K, V "
+                                    "[16, 8, 4096, 128]; Q [16, 32, 4096, 128]), static S, "
+                                    "swizzled scales", **onl,
+                        "hidden8192_us_per_call": table8,
+                        "importance_q_from_k_ms": round(ms_imp, 4)}
+    return out
 
 
 def main():
@@ -174,6 +248,8 @@ def main():
         "hbm_frac": round(alg_bytes / avg_launch_s / 1e9 / HBM_PEAK_GBS, 3),
     }
 
+    rows = None if args.no_rows else measure_rows(nv, workloads, torch, dev, layer)
+
     if args.copy_calibration:
         src = torch.empty(in_bytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
         dst = torch.empty_like(src)
@@ -223,6 +299,7 @@ def main():
         "cpu_baseline": cpu,
         "per_method": per_method,
         "per_method_single_calls": per_method_single,
+        "rows": rows,
         "time_vs_absmax": overhead,
     }
     print(json.dumps(line))
