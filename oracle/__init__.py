@@ -84,6 +84,9 @@ def _bind(lib):
         "nvfp4_ref_scales_bytes": (I64, [I64, I64, I, I]),
         "nvfp4_ref_quant_online": (I, [I, P, I, I64, I64, I, P, I64, I64, F, I, P, P, P]),
         "nvfp4_ref_channel_sq_norms": (I, [P, I, I64, I64, I64, I64, I64, I64, P]),
+        "nvfp4_ref_ldlq_order": (I, [P, I64, P]),
+        "nvfp4_ref_ldlq_factor": (I, [P, I64, D, P, P, P]),
+        "nvfp4_ref_ldlq": (I, [P, I, I64, I64, I, P, P, F, D, P]),
         "nvfp4_ref_tensor_scale": (I, [P, I, I64, F, P]),
         "nvfp4_ref_quantize": (I, [I, P, I, I64, I64, I, F, F, P, P, P, P]),
         "nvfp4_ref_dequant": (I, [P, P, F, I64, I64, I, P]),
@@ -377,3 +380,41 @@ def channel_sq_norms(x, group_rows: int = 1, groups: int = 1, group_div: int = 1
     if rc:
         raise OracleError(rc, "channel_sq_norms")
     return out
+
+
+# --- GPTQ / LDLQ with fixed block scales -----------------------------------------------------
+
+def ldlq_order(H) -> np.ndarray:
+    H = np.ascontiguousarray(H, dtype=np.float64)
+    perm = np.zeros(H.shape[0], dtype=np.int64)
+    rc = _load().nvfp4_ref_ldlq_order(_ptr(H), H.shape[0], _ptr(perm))
+    if rc:
+        raise OracleError(rc, "ldlq_order")
+    return perm
+
+
+def ldlq_factor(H, damp: float = 0.01, perm=None):
+    """(U strictly upper [n, n], D [n]) of the damped, reordered Hessian."""
+    H = np.ascontiguousarray(H, dtype=np.float64)
+    n = H.shape[0]
+    perm = ldlq_order(H) if perm is None else np.ascontiguousarray(perm, dtype=np.int64)
+    U = np.zeros((n, n))
+    D = np.zeros(n)
+    rc = _load().nvfp4_ref_ldlq_factor(_ptr(H), n, float(damp), _ptr(perm), _ptr(U), _ptr(D))
+    if rc:
+        raise OracleError(rc, "ldlq_factor")
+    return U, D
+
+
+def ldlq(w, H, scales, S: float, block: int = 16, damp: float = 0.01) -> np.ndarray:
+    """GPTQ (LDLQ form) nibbles [rows, n/2] with the given fixed block scales."""
+    w, dt = _tensor(w)
+    rows, n = w.shape
+    H = np.ascontiguousarray(H, dtype=np.float64)
+    sc = np.ascontiguousarray(scales, dtype=np.uint8)
+    q = np.zeros((rows, n // 2), dtype=np.uint8)
+    rc = _load().nvfp4_ref_ldlq(_ptr(w), dt, rows, n, block, _ptr(H), _ptr(sc), float(S),
+                                float(damp), _ptr(q))
+    if rc:
+        raise OracleError(rc, "ldlq")
+    return q

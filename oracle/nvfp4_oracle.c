@@ -549,6 +549,111 @@ int nvfp4_ref_channel_sq_norms(const void* x, int dtype, int64_t rows, int64_t c
     return REF_OK;
 }
 
+/* ------------------------------------------------------------------------------------- */
+/* GPTQ with fixed block scales (implementation details, GPTQ paragraph): LDLQ, damping    */
+/* 0.01 x the mean Hessian diagonal, static reordering by descending Hessian diagonal,     */
+/* block scales chosen before the pass.                                                   */
+/* ------------------------------------------------------------------------------------- */
+
+/* Column order of the pass: indices sorted by H_cc descending, ties by ascending index. */
+int nvfp4_ref_ldlq_order(const double* H, int64_t n, int64_t* perm)
+{
+    if (!H || !perm) return REF_ERR_NULL;
+    for (int64_t i = 0; i < n; ++i) perm[i] = i;
+    for (int64_t i = 1; i < n; ++i) {               /* insertion sort: stable */
+        int64_t v = perm[i];
+        double d = H[v * n + v];
+        int64_t j = i;
+        while (j > 0 && H[perm[j - 1] * n + perm[j - 1]] < d) {
+            perm[j] = perm[j - 1];
+            --j;
+        }
+        perm[j] = v;
+    }
+    return REF_OK;
+}
+
+/* Hp = P^T H P + lambda I with lambda = damp * (sum_c H_cc) / n (the diagonal summed in index
+ * order), P the column order; then Hp = (U + I) D (U + I)^T with U strictly upper triangular
+ * and D diagonal, computed from the last column backwards:
+ *   D_j  = Hp_jj - sum_{k > j} (U_jk U_jk) D_k
+ *   U_ij = (Hp_ij - sum_{k > j} (U_ik U_jk) D_k) / D_j      (i < j)
+ * each sum subtracted term by term from the largest k down.  U is returned row-major [n, n]
+ * (diagonal and lower part 0).  A non-positive or non-finite D_j is an error. */
+int nvfp4_ref_ldlq_factor(const double* H, int64_t n, double damp, const int64_t* perm,
+                          double* U, double* D)
+{
+    if (!H || !perm || !U || !D) return REF_ERR_NULL;
+    if (!(damp >= 0.0) || !isfinite(damp)) return REF_ERR_ARG;
+    double tr = 0.0;
+    for (int64_t c = 0; c < n; ++c) tr += H[c * n + c];
+    double lambda = n > 0 ? damp * (tr / (double)n) : 0.0;
+    for (int64_t i = 0; i < n * n; ++i) U[i] = 0.0;
+    for (int64_t j = n - 1; j >= 0; --j) {
+        double dj = H[perm[j] * n + perm[j]] + lambda;
+        for (int64_t k = n - 1; k > j; --k) dj = dj - (U[j * n + k] * U[j * n + k]) * D[k];
+        if (!(dj > 0.0) || !isfinite(dj)) return REF_ERR_ARG;
+        D[j] = dj;
+        for (int64_t i = 0; i < j; ++i) {
+            double acc = H[perm[i] * n + perm[j]];
+            for (int64_t k = n - 1; k > j; --k) acc = acc - (U[i * n + k] * U[j * n + k]) * D[k];
+            U[i * n + j] = acc / dj;
+        }
+    }
+    return REF_OK;
+}
+
+/* LDLQ (equivalent to GPTQ): in the column order, each column's values are
+ *   x_a = w_a + sum_{b < a} (w_b - w^_b) U_ba        (terms added from b = 0 up)
+ * and w^_a is x_a quantized with the block's fixed scale: y = RN32(RN32(x_a) / S), nibble =
+ * sign(y) << 3 | RNE_FP4(|y| / s), w^_a = +-E2M1 * s * S (exact in binary64).  w [rows, n]
+ * in binary32 or bfloat16, H [n, n] binary64, scales [rows, n / block] E4M3 codes fixed
+ * beforehand, S the global scale; q [rows, n / 2] nibbles as the quantizers pack them. */
+int nvfp4_ref_ldlq(const void* w, int dtype, int64_t rows, int64_t n, int block, const double* H,
+                   const uint8_t* scales, float S, double damp, uint8_t* q)
+{
+    if (dtype != 0 && dtype != 1) return REF_ERR_DTYPE;
+    if (!valid_block(block)) return REF_ERR_BLOCK;
+    if (rows < 0 || n < 0 || n % block != 0) return REF_ERR_SHAPE;
+    if (!(S > 0.0f) || !isfinite(S)) return REF_ERR_ARG;
+    if (rows * n > 0 && (!w || !H || !scales || !q)) return REF_ERR_NULL;
+    if (n == 0 || rows == 0) return REF_OK;
+    int64_t* perm = (int64_t*)malloc((size_t)n * sizeof(int64_t));
+    double* U = (double*)malloc((size_t)(n * n) * sizeof(double));
+    double* D = (double*)malloc((size_t)n * sizeof(double));
+    double* e = (double*)malloc((size_t)n * sizeof(double));
+    int rc = (perm && U && D && e) ? REF_OK : REF_ERR_ARG;
+    if (rc == REF_OK) rc = nvfp4_ref_ldlq_order(H, n, perm);
+    if (rc == REF_OK) rc = nvfp4_ref_ldlq_factor(H, n, damp, perm, U, D);
+    int64_t nb = n / block;
+    for (int64_t r = 0; r < rows && rc == REF_OK; ++r) {
+        for (int64_t a = 0; a < n; ++a) {
+            int64_t c = perm[a];
+            double wv = (double)load_elem(w, dtype, r * n + c);
+            double x = wv;
+            for (int64_t b = 0; b < a; ++b) x = x + e[b] * U[b * n + a];
+            float y = (float)x / S;
+            double s = nvfp4_ref_e4m3(scales[r * nb + c / block]);
+            int k = nvfp4_ref_round_fp4(fabs((double)y), s);
+            double wq = nvfp4_ref_e2m1(k) * s * (double)S;
+            if (signbit(y)) wq = -wq;
+            e[a] = wv - wq;
+            int nib = (signbit(y) ? 8 : 0) | k;
+            int64_t el = r * n + c;
+            uint8_t* byte = &q[el >> 1];
+            if ((el & 1) == 0)
+                *byte = (uint8_t)((*byte & 0xF0) | nib);
+            else
+                *byte = (uint8_t)((*byte & 0x0F) | (nib << 4));
+        }
+    }
+    free(perm);
+    free(U);
+    free(D);
+    free(e);
+    return rc;
+}
+
 int nvfp4_ref_quant_absmax(const void* x, int dtype, int64_t rows, int64_t cols, int block,
                            float fp8_range, float static_scale, float* tensor_scale,
                            uint8_t* q, uint8_t* scales)

@@ -94,6 +94,12 @@ int nvfp4_ref_quant_online(int method, const void* x, int dtype, int64_t rows, i
 int nvfp4_ref_channel_sq_norms(const void* x, int dtype, int64_t rows, int64_t cols,
                                int64_t group_rows, int64_t groups, int64_t group_div,
                                int64_t rep_out, float* out);
+/* GPTQ / LDLQ with fixed block scales (implementation details, GPTQ paragraph). */
+int nvfp4_ref_ldlq_order(const double* H, int64_t n, int64_t* perm);
+int nvfp4_ref_ldlq_factor(const double* H, int64_t n, double damp, const int64_t* perm,
+                          double* U, double* D);
+int nvfp4_ref_ldlq(const void* w, int dtype, int64_t rows, int64_t n, int block, const double* H,
+                   const uint8_t* scales, float S, double damp, uint8_t* q);
 int nvfp4_ref_dequant(const uint8_t* q, const uint8_t* scales, float tensor_scale,
                       int64_t rows, int64_t cols, int block, float* out);
 

@@ -60,6 +60,12 @@ MUTANTS = [
      "importance + (r % imp_groups) * cols"),
     ("optimum_piece_at_low_end", "double s_ref = (seg == 0) ? 0.5 * hi : (seg == nb) ? 2.0 * lo : 0.5 * (lo + hi);",
      "double s_ref = (seg == 0) ? 0.5 * hi : (seg == nb) ? 2.0 * lo : lo;"),
+    ("ldlq_order_ascending", "while (j > 0 && H[perm[j - 1] * n + perm[j - 1]] < d) {",
+     "while (j > 0 && H[perm[j - 1] * n + perm[j - 1]] > d) {"),
+    ("ldlq_no_damping", "double lambda = n > 0 ? damp * (tr / (double)n) : 0.0;",
+     "double lambda = 0.0 * damp * tr;"),
+    ("ldlq_feedback_sign", "for (int64_t b = 0; b < a; ++b) x = x + e[b] * U[b * n + a];",
+     "for (int64_t b = 0; b < a; ++b) x = x - e[b] * U[b * n + a];"),
     ("fp8_opt_ceil_not_taken", "if (nvfp4_ref_e4m3(cf) < s_opt && cf < E4M3_MAX_CODE) cc = cf + 1;",
      "if (nvfp4_ref_e4m3(cf) < s_opt && cf < E4M3_MAX_CODE) cc = cf;"),
 ]
@@ -79,6 +85,7 @@ def test_planted_mistake_is_caught(name, orig, planted, tmp_path):
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         "-m", "not slow", "tests/test_oracle_pins.py",
                         "tests/test_oracle_bruteforce.py", "tests/test_oracle_windows.py",
-                        "tests/test_oracle_optimum.py", "tests/test_oracle_online.py"],
+                        "tests/test_oracle_optimum.py", "tests/test_oracle_online.py",
+                        "tests/test_oracle_ldlq.py"],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"planted mistake {name} was not caught:\n{r.stdout[-2000:]}"
