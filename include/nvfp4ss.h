@@ -206,6 +206,26 @@ int nvfp4_channel_sq_norms(const void* x, int dtype, int64_t rows, int64_t cols,
                            int64_t groups, int64_t group_div, int64_t rep_out, float* out,
                            void* workspace, size_t workspace_bytes, void* stream);
 
+/* GPTQ with fixed block scales (implementation details, GPTQ paragraph), in the LDLQ form the
+ * paper uses: the block scales (scales [rows, cols/block] E4M3 codes, row-major) and the
+ * global scale (*tensor_scale, device) are chosen beforehand by a quantizer call; the input
+ * channels are visited in descending order of the Hessian diagonal (ties by index); the
+ * Hessian hessian [cols, cols] (binary64, row-major, symmetric positive semi-definite, e.g.
+ * X^T X over calibration activations) is damped by damp x its mean diagonal (damp = 0.01 in
+ * the paper) and factored as (U + I) D (U + I)^T with U strictly upper triangular; then each
+ * value, in that order, is its weight plus the earlier errors (w - w^) times U, quantized with
+ * its block's fixed scale as the quantizers round: y = RN32(RN32(x) / S), nibble
+ * sign(y) << 3 | RNE_FP4(|y| / s).  Outputs q [rows, cols/2] nibbles as the quantizers pack
+ * them.  w: [rows, cols] binary32 or bfloat16.  cols must be a multiple of 64.  *status
+ * (device int) is set to 0, or 1 if the damped Hessian is not positive definite (then q is
+ * unspecified): check it after synchronizing.  workspace: >= nvfp4_ldlq_workspace_bytes()
+ * bytes (about 8 (cols^2 + 2 rows cols) bytes), 256-byte aligned, no initialization.  All
+ * arithmetic is binary64 in a fixed order (no atomics), so results are deterministic. */
+size_t nvfp4_ldlq_workspace_bytes(int64_t rows, int64_t cols);
+int nvfp4_ldlq(const void* w, int dtype, int64_t rows, int64_t cols, int block, const double* hessian,
+               const uint8_t* scales, const float* tensor_scale, double damp, uint8_t* q, int* status,
+               void* workspace, size_t workspace_bytes, void* stream);
+
 /* One tensor of a batched call: device pointers and shape, as in the single-tensor calls
  * (col_weight: NULL unless the method uses weights). */
 typedef struct {

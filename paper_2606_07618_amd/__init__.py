@@ -13,6 +13,8 @@ from .nvfp4 import (  # noqa: F401
     channel_sq_norms,
     dequant,
     gap_report,
+    gptq_quantize,
+    ldlq,
     lib,
     nvfp4_batched_workspace_bytes,
     nvfp4_block_loss,
@@ -20,6 +22,8 @@ from .nvfp4 import (  # noqa: F401
     nvfp4_channel_sq_norms,
     nvfp4_channel_sq_norms_workspace_bytes,
     nvfp4_dequant,
+    nvfp4_ldlq,
+    nvfp4_ldlq_workspace_bytes,
     nvfp4_quant_batched,
     nvfp4_quant_absmax,
     nvfp4_quant_four_over_six,

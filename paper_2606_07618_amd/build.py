@@ -8,7 +8,8 @@ from pathlib import Path
 HERE = Path(__file__).resolve().parent
 ROOT = HERE.parent
 SRC = HERE / "csrc" / "nvfp4ss.hip"
-SOURCES = [SRC, HERE / "csrc" / "optimum.hip", HERE / "csrc" / "importance.hip"]
+SOURCES = [SRC, HERE / "csrc" / "optimum.hip", HERE / "csrc" / "importance.hip",
+           HERE / "csrc" / "gptq.hip"]
 LIB = HERE / "libnvfp4ss.so"
 
 HIPCC_FLAGS = [

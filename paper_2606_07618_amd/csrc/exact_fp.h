@@ -1,0 +1,54 @@
+// Exact FP4 / FP8 helpers in binary64 shared by the analysis and GPTQ kernels: E2M1 values and
+// the midpoints between them, E4M3 code values, and the nearest-E2M1 index of a / s by exact
+// comparisons (NVFP4 section; Appendix A for the formats).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+
+namespace nvfp4_exact {
+
+// Midpoints between consecutive E2M1 magnitudes {0, 0.5, 1, 1.5, 2, 3, 4, 6}.
+__device__ __forceinline__ double e2m1_mid(int k) {
+    return k == 0 ? 0.25 : k == 1 ? 0.75 : k == 2 ? 1.25 : k == 3 ? 1.75
+         : k == 4 ? 2.5 : k == 5 ? 3.5 : 5.0;
+}
+
+__device__ __forceinline__ double e2m1_value(int k) {
+    return k == 0 ? 0.0 : k == 1 ? 0.5 : k == 2 ? 1.0 : k == 3 ? 1.5
+         : k == 4 ? 2.0 : k == 5 ? 3.0 : k == 6 ? 4.0 : 6.0;
+}
+
+// E4M3 code c = a * 8 + b (0..126): 2^(a - 7) (1 + b/8) for a > 0, 2^-6 (b/8) for a = 0.
+__device__ __forceinline__ double e4m3_f64(int c) {
+    const int a = c >> 3, b = c & 7;
+    return a ? ldexp(1.0 + 0.125 * b, a - 7) : ldexp(0.125 * b, -6);
+}
+
+// Index of the E2M1 value nearest to a / s (a >= 0, s > 0): the number of midpoints m_k with
+// a > m_k s, where a midpoint that a meets exactly counts only if it leads to an even code.
+// The products m_k s are rounded once in binary64 (exact when s is an E4M3 value).
+__device__ __forceinline__ int round_fp4_index(double a, double s) {
+    if (s == 0.0) return 0;
+    int k = 0;
+#pragma unroll
+    for (int j = 0; j < 7; ++j) {
+        const double m = e2m1_mid(j) * s;
+        const bool up = a > m || (a == m && ((j + 1) & 1) == 0);
+        k = (k == j && up) ? j + 1 : k;
+    }
+    return k;
+}
+
+// Largest code c in 0..126 with E4M3(c) <= v (v >= 0; +inf gives 126).
+__device__ __forceinline__ int floor_e4m3(double v) {
+    int lo = 0, hi = 126;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (e4m3_f64(mid) <= v) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+}
+
+}  // namespace nvfp4_exact

@@ -1,0 +1,409 @@
+// GPTQ with fixed NVFP4 block scales on AMD Instinct MI355X (gfx950), in its LDLQ form
+// (implementation details, GPTQ paragraph): the block scales are chosen before the pass (by
+// any of the quantizers), the input channels are visited in descending order of the Hessian
+// diagonal, the Hessian is damped by 0.01 x its mean diagonal, and
+//   x_a = w_a + sum_{b < a} (w_b - w^_b) U_ba,     w^_a = Q(x_a)
+// with Hp = (U + I) D (U + I)^T the factorization of the damped, reordered Hessian (U strictly
+// upper triangular).  LDLQ and GPTQ give the same result.  Everything is binary64 with a
+// fixed order of correctly rounded operations per value:
+//   * factor: Hp is factored in place (column-major) in 64-column blocks from the last:
+//     the block's own columns in LDS, one column at a time from its last; then the rows
+//     above it, each a 64-column triangular solve; then the block's contribution
+//     (U_ik U_jk) D_k, k walked downwards, is subtracted from the rest of the upper triangle
+//     in 64 x 64 tiles.  So each element receives its terms k = n-1, ..., j+1 in that order.
+//   * quantize: columns are taken in tiles of 64.  A tile kernel gives each row one lane that
+//     walks the tile in order: x_a is its running value plus the products of the tile's
+//     earlier errors (LDS) with U (staged in LDS), added in order; then x_a is quantized and
+//     its error kept.  A trailing-update kernel then adds the tile's 64 errors times U to every
+//     later column, term by term in tile order, in 64 x 64 output blocks with 4 x 4 values
+//     per lane.  Every x_a therefore receives its terms b = 0, 1, ... in ascending order, as
+//     the sequential definition adds them.
+// Q(x) is the quantizers' rounding: y = RN32(RN32(x) / S), nibble sign(y) << 3 | RNE_FP4(|y| /
+// s), w^ = +-E2M1 * s * S (exact in binary64).
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+
+#include "exact_fp.h"
+#include "nvfp4ss.h"
+
+namespace {
+
+using namespace nvfp4_exact;
+
+constexpr int kTile = 64;
+
+template <typename In>
+__device__ __forceinline__ float load_w(const In* w, int64_t i);
+
+template <>
+__device__ __forceinline__ float load_w<float>(const float* w, int64_t i) { return w[i]; }
+
+template <>
+__device__ __forceinline__ float load_w<uint16_t>(const uint16_t* w, int64_t i) {
+    return __uint_as_float((uint32_t)w[i] << 16);
+}
+
+// ---- column order and damping ------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void diag_kernel(const double* __restrict__ H, int64_t n,
+                                                   double* __restrict__ diag) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n) diag[i] = H[i * n + i];
+}
+
+// perm[rank(i)] = i, rank = number of columns with a larger diagonal, or an equal one and a
+// smaller index (a stable descending order).
+__global__ __launch_bounds__(256) void order_kernel(const double* __restrict__ diag, int64_t n,
+                                                    int* __restrict__ perm) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    const double d = diag[i];
+    int64_t rank = 0;
+    for (int64_t j = 0; j < n; ++j) {
+        const double e = diag[j];
+        rank += (e > d || (e == d && j < i)) ? 1 : 0;
+    }
+    perm[rank] = (int)i;
+}
+
+// lambda = damp * (sum of the diagonal in index order) / n, one lane.
+__global__ void damping_kernel(const double* __restrict__ diag, int64_t n, double damp,
+                               double* __restrict__ lambda) {
+    double tr = 0.0;
+    for (int64_t c = 0; c < n; ++c) tr += diag[c];
+    lambda[0] = damp * (tr / (double)n);
+}
+
+// ---- factor: blocked, from the last 64-column block backwards ---------------------------
+// Uc holds A = Hp column-major (Uc[j n + i] = A_ij for i <= j) and is overwritten in place by
+// U.  Element (i, j) must receive its terms k = n-1, n-2, ..., j+1 in that order; the blocks
+// are finished last-first and every kernel walks k downwards, so it does.
+
+__global__ __launch_bounds__(256) void init_a_kernel(const double* __restrict__ H,
+                                                     const int* __restrict__ perm,
+                                                     const double* __restrict__ lambda, int64_t n,
+                                                     double* __restrict__ Uc) {
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t >= n * n) return;
+    const int64_t j = t / n, i = t % n;
+    double v = H[(int64_t)perm[i] * n + perm[j]];
+    if (i == j) v = v + lambda[0];
+    Uc[t] = v;
+}
+
+// The diagonal block [k0, k0 + 64): its D and its U, column by column from the last, in LDS.
+__global__ __launch_bounds__(kTile) void factor_diag_kernel(double* __restrict__ Uc, double* __restrict__ D,
+                                                            int64_t n, int64_t k0, int* __restrict__ status) {
+    __shared__ double Ab[kTile][kTile + 1];   // Ab[ii][jj]: A, then U, of (k0 + ii, k0 + jj)
+    __shared__ double Db[kTile];
+    const int lane = threadIdx.x;
+    for (int jj = 0; jj < kTile; ++jj) Ab[lane][jj] = Uc[(k0 + jj) * n + k0 + lane];
+    __syncthreads();
+    for (int jj = kTile - 1; jj >= 0; --jj) {
+        if (lane == 0) {
+            double d = Ab[jj][jj];
+            for (int kk = kTile - 1; kk > jj; --kk) {
+                const double u = Ab[jj][kk];
+                d = d - (u * u) * Db[kk];
+            }
+            Db[jj] = d;
+        }
+        double acc = Ab[lane][jj];
+        for (int kk = kTile - 1; kk > jj; --kk) acc = acc - (Ab[lane][kk] * Ab[jj][kk]) * Db[kk];
+        __syncthreads();
+        if (lane < jj) Ab[lane][jj] = acc / Db[jj];
+        __syncthreads();
+    }
+    for (int jj = lane + 1; jj < kTile; ++jj) Uc[(k0 + jj) * n + k0 + lane] = Ab[lane][jj];
+    const double d = Db[lane];
+    D[k0 + lane] = d;
+    if (!(d > 0.0) || !isfinite(d)) status[0] = 1;               // not positive definite
+}
+
+// Rows above the block (i < k0), 64 per workgroup: U_ij for the block's columns, each row a
+// triangular solve from the block's last column, with the row's new values kept in LDS.
+__global__ __launch_bounds__(kTile) void factor_panel_kernel(double* __restrict__ Uc,
+                                                             const double* __restrict__ D, int64_t n,
+                                                             int64_t k0) {
+    __shared__ double Ub[kTile][kTile + 1];   // Ub[jj][kk] = U_{k0+jj, k0+kk}, jj < kk
+    __shared__ double ui[kTile][kTile];       // ui[kk][lane] = U_{i, k0+kk}
+    __shared__ double Db[kTile];
+    const int lane = threadIdx.x;
+    for (int kk = 0; kk < kTile; ++kk) Ub[lane][kk] = Uc[(k0 + kk) * n + k0 + lane];
+    Db[lane] = D[k0 + lane];
+    __syncthreads();
+    const int64_t i = (int64_t)blockIdx.x * kTile + lane;
+    if (i >= k0) return;
+    for (int jj = kTile - 1; jj >= 0; --jj) {
+        double acc = Uc[(k0 + jj) * n + i];
+        for (int kk = kTile - 1; kk > jj; --kk) acc = acc - (ui[kk][lane] * Ub[jj][kk]) * Db[kk];
+        const double u = acc / Db[jj];
+        ui[jj][lane] = u;
+        Uc[(k0 + jj) * n + i] = u;
+    }
+}
+
+// A_ij -= sum over the block's k, downwards, of (U_ik U_jk) D_k for i <= j < k0: one 64 x 64
+// tile of the upper triangle per workgroup (tiles below it exit), 4 x 4 values per lane.
+__global__ __launch_bounds__(256) void factor_trailing_kernel(double* __restrict__ Uc,
+                                                              const double* __restrict__ D,
+                                                              int64_t n, int64_t k0) {
+    const int64_t bi = blockIdx.y, bj = blockIdx.x;
+    if (bi > bj) return;
+    __shared__ double Ui[kTile][kTile + 1];   // Ui[ii][kk] = U_{i0+ii, k0+kk}
+    __shared__ double Uj[kTile][kTile + 1];
+    __shared__ double Dk[kTile];
+    const int64_t i0 = bi * kTile, j0 = bj * kTile;
+    for (int t = threadIdx.x; t < kTile * kTile; t += 256) {
+        const int kk = t / kTile, r = t % kTile;                  // coalesced over r
+        Ui[r][kk] = Uc[(k0 + kk) * n + i0 + r];
+        Uj[r][kk] = Uc[(k0 + kk) * n + j0 + r];
+    }
+    if (threadIdx.x < kTile) Dk[threadIdx.x] = D[k0 + threadIdx.x];
+    __syncthreads();
+    const int tr = threadIdx.x / 16, tc = threadIdx.x % 16;
+    double acc[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = Uc[(j0 + tc + 16 * b) * n + i0 + tr + 16 * a];
+    for (int kk = kTile - 1; kk >= 0; --kk) {
+        double ua[4], ub[4];
+#pragma unroll
+        for (int a = 0; a < 4; ++a) ua[a] = Ui[tr + 16 * a][kk];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) ub[b] = Uj[tc + 16 * b][kk];
+        const double dk = Dk[kk];
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int b = 0; b < 4; ++b) acc[a][b] = acc[a][b] - (ua[a] * ub[b]) * dk;
+    }
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int64_t i = i0 + tr + 16 * a, j = j0 + tc + 16 * b;
+            if (i <= j) Uc[j * n + i] = acc[a][b];
+        }
+}
+
+// ---- quantize -----------------------------------------------------------------------------
+
+template <typename In>
+__global__ __launch_bounds__(256) void init_x_kernel(const In* __restrict__ w, const int* __restrict__ perm,
+                                                     int64_t rows, int64_t n, double* __restrict__ X) {
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t >= rows * n) return;
+    const int64_t r = t / n, a = t % n;
+    X[t] = (double)load_w<In>(w, r * n + perm[a]);
+}
+
+// One lane per row (64 rows per workgroup), walking the tile in order: value a of the tile is
+// its running value from X plus the products of the tile's earlier errors (kept in LDS, one
+// column per lane) with U, added from b = a0 up; then it is quantized and its error stored.
+template <typename In>
+__global__ __launch_bounds__(kTile) void tile_kernel(const In* __restrict__ w, const int* __restrict__ perm,
+                                                     const double* __restrict__ Uc,
+                                                     const uint8_t* __restrict__ scales,
+                                                     const float* __restrict__ tensor_scale,
+                                                     int64_t rows, int64_t n, int block, int64_t a0,
+                                                     const double* __restrict__ X,
+                                                     double* __restrict__ Et,
+                                                     uint8_t* __restrict__ codes) {
+    __shared__ double T[kTile][kTile];      // T[b][a] = U_{a0+b, a0+a}
+    __shared__ double es[kTile][kTile];     // es[b][lane]: error of tile column b, this lane's row
+    __shared__ int pc[kTile];
+    const int lane = threadIdx.x;
+#pragma unroll 8
+    for (int a = 0; a < kTile; ++a) T[lane][a] = Uc[(a0 + a) * n + a0 + lane];   // coalesced
+    pc[lane] = perm[a0 + lane];
+    __syncthreads();
+    const int64_t r = (int64_t)blockIdx.x * kTile + lane;
+    if (r >= rows) return;
+    const float S = tensor_scale[0];
+    const double Sd = (double)S;
+    const int64_t nb = n / block;
+#pragma unroll 1
+    for (int a = 0; a < kTile; ++a) {
+        double x = X[r * n + a0 + a];
+#pragma unroll 4
+        for (int b = 0; b < a; ++b) x = x + es[b][lane] * T[b][a];
+        const int c = pc[a];
+        const double wv = (double)load_w<In>(w, r * n + c);
+        const float y = __fdiv_rn(__double2float_rn(x), S);
+        const double s = e4m3_f64(scales[r * nb + c / block]);
+        const int k = round_fp4_index(fabs((double)y), s);
+        double wq = e2m1_value(k) * s * Sd;
+        const bool neg = signbit(y);
+        if (neg) wq = -wq;
+        const double e = wv - wq;
+        codes[r * n + c] = (uint8_t)((neg ? 8 : 0) | k);
+        es[a][lane] = e;
+        Et[r * kTile + a] = e;
+    }
+}
+
+// X[r][k] += sum over the tile's b (in order) of Et[r][b] * U_{a0+b, k}, for k >= a0 + 64:
+// one 64 x 64 output block per workgroup, 4 x 4 values per lane.
+__global__ __launch_bounds__(256) void trailing_kernel(const double* __restrict__ Et,
+                                                       const double* __restrict__ Uc,
+                                                       int64_t rows, int64_t n, int64_t a0,
+                                                       double* __restrict__ X) {
+    __shared__ double Es[kTile][kTile + 1];    // Es[row][b]
+    __shared__ double Us[kTile][kTile + 1];    // Us[b][col]
+    const int64_t r0 = (int64_t)blockIdx.y * kTile;
+    const int64_t k0 = a0 + kTile + (int64_t)blockIdx.x * kTile;
+    for (int t = threadIdx.x; t < kTile * kTile; t += 256) {
+        const int rr = t / kTile, b = t % kTile;
+        Es[rr][b] = r0 + rr < rows ? Et[(r0 + rr) * kTile + b] : 0.0;
+        const int cc = t / kTile, bb = t % kTile;                 // coalesced over b
+        Us[bb][cc] = k0 + cc < n ? Uc[(k0 + cc) * n + a0 + bb] : 0.0;
+    }
+    __syncthreads();
+    const int tr = threadIdx.x / 16, tc = threadIdx.x % 16;      // 16 x 16 lanes, 4 x 4 each
+    double acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t r = r0 + tr + 16 * i, k = k0 + tc + 16 * j;
+            acc[i][j] = (r < rows && k < n) ? X[r * n + k] : 0.0;
+        }
+    for (int b = 0; b < kTile; ++b) {
+        double e[4], u[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) e[i] = Es[tr + 16 * i][b];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) u[j] = Us[b][tc + 16 * j];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = acc[i][j] + e[i] * u[j];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t r = r0 + tr + 16 * i, k = k0 + tc + 16 * j;
+            if (r < rows && k < n) X[r * n + k] = acc[i][j];
+        }
+}
+
+__global__ __launch_bounds__(256) void pack_kernel(const uint8_t* __restrict__ codes, int64_t npairs,
+                                                   uint8_t* __restrict__ q) {
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t < npairs) q[t] = (uint8_t)(codes[2 * t] | (codes[2 * t + 1] << 4));
+}
+
+__global__ void clear_status_kernel(int* status) { status[0] = 0; }
+
+// ---- workspace ---------------------------------------------------------------------------
+
+struct Layout {
+    size_t perm, diag, lambda, D, Uc, X, Et, codes, total;
+};
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+Layout layout_of(int64_t rows, int64_t n) {
+    Layout l;
+    size_t o = 0;
+    l.perm = o;   o = align256(o + (size_t)n * sizeof(int));
+    l.diag = o;   o = align256(o + (size_t)n * sizeof(double));
+    l.lambda = o; o = align256(o + sizeof(double));
+    l.D = o;      o = align256(o + (size_t)n * sizeof(double));
+    l.Uc = o;     o = align256(o + (size_t)n * n * sizeof(double));
+    l.X = o;      o = align256(o + (size_t)rows * n * sizeof(double));
+    l.Et = o;     o = align256(o + (size_t)rows * kTile * sizeof(double));
+    l.codes = o;  o = align256(o + (size_t)rows * n);
+    l.total = o;
+    return l;
+}
+
+unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+template <typename In>
+int run_ldlq(const void* wv, int64_t rows, int64_t n, int block, const double* H,
+             const uint8_t* scales, const float* S, double damp, uint8_t* q, int* status,
+             char* ws, hipStream_t st) {
+    const In* w = static_cast<const In*>(wv);
+    const Layout l = layout_of(rows, n);
+    int* perm = reinterpret_cast<int*>(ws + l.perm);
+    double* diag = reinterpret_cast<double*>(ws + l.diag);
+    double* lambda = reinterpret_cast<double*>(ws + l.lambda);
+    double* D = reinterpret_cast<double*>(ws + l.D);
+    double* Uc = reinterpret_cast<double*>(ws + l.Uc);
+    double* X = reinterpret_cast<double*>(ws + l.X);
+    double* Et = reinterpret_cast<double*>(ws + l.Et);
+    uint8_t* codes = reinterpret_cast<uint8_t*>(ws + l.codes);
+
+    hipLaunchKernelGGL(clear_status_kernel, dim3(1), dim3(1), 0, st, status);
+    hipLaunchKernelGGL(diag_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, H, n, diag);
+    hipLaunchKernelGGL(order_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, diag, n, perm);
+    hipLaunchKernelGGL(damping_kernel, dim3(1), dim3(1), 0, st, diag, n, damp, lambda);
+    if (hipGetLastError() != hipSuccess) return NVFP4_ERR_HIP;
+    hipLaunchKernelGGL(init_a_kernel, dim3(blocks_for(n * n, 256)), dim3(256), 0, st, H, perm, lambda,
+                       n, Uc);
+    for (int64_t k0 = n - kTile; k0 >= 0; k0 -= kTile) {
+        hipLaunchKernelGGL(factor_diag_kernel, dim3(1), dim3(kTile), 0, st, Uc, D, n, k0, status);
+        if (k0 > 0) {
+            hipLaunchKernelGGL(factor_panel_kernel, dim3(blocks_for(k0, kTile)), dim3(kTile), 0, st, Uc,
+                               D, n, k0);
+            const unsigned tiles = (unsigned)(k0 / kTile);
+            hipLaunchKernelGGL(factor_trailing_kernel, dim3(tiles, tiles), dim3(256), 0, st, Uc, D, n, k0);
+        }
+        if (hipGetLastError() != hipSuccess) return NVFP4_ERR_HIP;
+    }
+    hipLaunchKernelGGL(init_x_kernel<In>, dim3(blocks_for(rows * n, 256)), dim3(256), 0, st, w, perm,
+                       rows, n, X);
+    for (int64_t a0 = 0; a0 < n; a0 += kTile) {
+        hipLaunchKernelGGL(tile_kernel<In>, dim3(blocks_for(rows, kTile)), dim3(kTile), 0, st, w, perm, Uc,
+                           scales, S, rows, n, block, a0, X, Et, codes);
+        const int64_t rest = n - a0 - kTile;
+        if (rest > 0)
+            hipLaunchKernelGGL(trailing_kernel, dim3(blocks_for(rest, kTile), blocks_for(rows, kTile)),
+                               dim3(256), 0, st, Et, Uc, rows, n, a0, X);
+        if (hipGetLastError() != hipSuccess) return NVFP4_ERR_HIP;
+    }
+    hipLaunchKernelGGL(pack_kernel, dim3(blocks_for(rows * n / 2, 256)), dim3(256), 0, st, codes,
+                       rows * n / 2, q);
+    return hipGetLastError() == hipSuccess ? NVFP4_OK : NVFP4_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t nvfp4_ldlq_workspace_bytes(int64_t rows, int64_t cols) {
+    if (rows < 0 || cols < 0) return 0;
+    return layout_of(rows, cols).total;
+}
+
+int nvfp4_ldlq(const void* w, int dtype, int64_t rows, int64_t cols, int block, const double* hessian,
+               const uint8_t* scales, const float* tensor_scale, double damp, uint8_t* q, int* status,
+               void* workspace, size_t workspace_bytes, void* stream) {
+    if (dtype != NVFP4_IN_F32 && dtype != NVFP4_IN_BF16) return NVFP4_ERR_DTYPE;
+    if (block != 16 && block != 32 && block != 64 && block != 128) return NVFP4_ERR_BLOCK;
+    if (rows < 0 || cols < 0 || cols % kTile != 0) return NVFP4_ERR_SHAPE;
+    if (cols > 0x7FFFFFFF || rows * cols > ((int64_t)1 << 40)) return NVFP4_ERR_SHAPE;
+    if (!(damp >= 0.0) || !isfinite(damp)) return NVFP4_ERR_ARG;
+    if (!status || !tensor_scale) return NVFP4_ERR_NULL;
+    if (rows * cols > 0 && (!w || !hessian || !scales || !q)) return NVFP4_ERR_NULL;
+    if (((uintptr_t)hessian & 7) || ((uintptr_t)status & 3)) return NVFP4_ERR_ALIGN;
+    hipStream_t st = (hipStream_t)stream;
+    if (rows * cols == 0) {
+        hipLaunchKernelGGL(clear_status_kernel, dim3(1), dim3(1), 0, st, status);
+        return hipGetLastError() == hipSuccess ? NVFP4_OK : NVFP4_ERR_HIP;
+    }
+    if (!workspace || workspace_bytes < layout_of(rows, cols).total) return NVFP4_ERR_WORKSPACE;
+    if ((uintptr_t)workspace & 255) return NVFP4_ERR_ALIGN;
+    char* ws = static_cast<char*>(workspace);
+    return dtype == NVFP4_IN_F32
+        ? run_ldlq<float>(w, rows, cols, block, hessian, scales, tensor_scale, damp, q, status, ws, st)
+        : run_ldlq<uint16_t>(w, rows, cols, block, hessian, scales, tensor_scale, damp, q, status, ws, st);
+}
+
+}  // extern "C"

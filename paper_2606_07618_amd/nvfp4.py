@@ -52,6 +52,8 @@ def _load():
         "nvfp4_quant_online": (I, [I, P, I, I64, I64, I, P, I64, I64, F, I, P, P, P, P]),
         "nvfp4_channel_sq_norms_workspace_bytes": (I64, [I64, I64, I64, I64]),
         "nvfp4_channel_sq_norms": (I, [P, I, I64, I64, I64, I64, I64, I64, P, P, SZ, P]),
+        "nvfp4_ldlq_workspace_bytes": (SZ, [I64, I64]),
+        "nvfp4_ldlq": (I, [P, I, I64, I64, I, P, P, P, ctypes.c_double, P, P, P, SZ, P]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(L, name)
@@ -86,6 +88,8 @@ nvfp4_scales_bytes = lib.nvfp4_scales_bytes
 nvfp4_quant_online = lib.nvfp4_quant_online
 nvfp4_channel_sq_norms_workspace_bytes = lib.nvfp4_channel_sq_norms_workspace_bytes
 nvfp4_channel_sq_norms = lib.nvfp4_channel_sq_norms
+nvfp4_ldlq_workspace_bytes = lib.nvfp4_ldlq_workspace_bytes
+nvfp4_ldlq = lib.nvfp4_ldlq
 nvfp4_batched_workspace_bytes = lib.nvfp4_batched_workspace_bytes
 nvfp4_quant_batched = lib.nvfp4_quant_batched
 METHOD_IDS = {"absmax": 0, "four_over_six": 1, "scalesweep_mse": 2, "scalesweep_wmse": 3}
@@ -399,3 +403,44 @@ def channel_sq_norms(x: torch.Tensor, group_rows: int = 1, groups: int = 1, grou
     if rc != 0:
         raise NVFP4Error(rc, "nvfp4_channel_sq_norms")
     return out
+
+
+# ---- GPTQ (LDLQ form) with fixed block scales ----------------------------------------------
+
+def ldlq(w: torch.Tensor, hessian: torch.Tensor, scales: torch.Tensor, S: torch.Tensor,
+         block: int = 16, damp: float = 0.01, check: bool = True) -> torch.Tensor:
+    """GPTQ nibbles [rows, cols/2] of w with the given fixed scales (see nvfp4_ldlq).
+    hessian: [cols, cols] float64 device tensor.  With ``check`` the call synchronizes and
+    raises if the damped Hessian is not positive definite."""
+    dt = _check_input(w)
+    _check_scale(S, w.device)
+    rows, cols = w.shape
+    if not (hessian.is_cuda and hessian.dtype == torch.float64 and hessian.is_contiguous()
+            and tuple(hessian.shape) == (cols, cols)):
+        raise ValueError("hessian must be a contiguous float64 device tensor [cols, cols]")
+    if not (scales.is_cuda and scales.dtype == torch.uint8 and scales.is_contiguous()
+            and scales.numel() == rows * (cols // block)):
+        raise ValueError("scales must be a contiguous uint8 device tensor [rows, cols/block]")
+    nbytes = nvfp4_ldlq_workspace_bytes(rows, cols)
+    ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=w.device)
+    q = torch.empty((rows, cols // 2), dtype=torch.uint8, device=w.device)
+    status = torch.empty(1, dtype=torch.int32, device=w.device)
+    rc = nvfp4_ldlq(_ptr(w), dt, rows, cols, block, _ptr(hessian), _ptr(scales), _ptr(S),
+                    ctypes.c_double(damp), _ptr(q), _ptr(status), _ptr(ws), nbytes,
+                    _stream(w.device))
+    if rc != 0:
+        raise NVFP4Error(rc, "nvfp4_ldlq")
+    if check and int(status.item()) != 0:
+        raise NVFP4Error(-5, "nvfp4_ldlq: the damped Hessian is not positive definite")
+    return q
+
+
+def gptq_quantize(w: torch.Tensor, hessian: torch.Tensor, method: str = "scalesweep_wmse",
+                  block: int = 16, damp: float = 0.01):
+    """The paper's GPTQ pipeline for one weight: block scales by ``method`` first (WMSE
+    importance = the Hessian diagonal), then the LDLQ pass with those scales fixed.
+    Returns (q, scales, S)."""
+    imp = torch.diagonal(hessian).to(torch.float32).contiguous()
+    wm = imp if method in ("four_over_six", "scalesweep_wmse") else None
+    _, sc, S = quantize(w, method, block, weight=wm)
+    return ldlq(w, hessian, sc, S, block, damp), sc, S

@@ -216,3 +216,26 @@ def test_channel_norms_validation(nv):
     assert f(FAKE, 1, 512, 64, 1, 8, 2, 1, None, FAKE8, wsb, None) == -1
     assert f(FAKE, 1, 512, 64, 1, 8, 2, 1, FAKE, FAKE8, wsb - 8, None) == -6
     assert f(FAKE, 1, 512, 64, 1, 8, 2, 1, FAKE, P(0x100004), wsb, None) == -7
+
+
+def test_ldlq_validation(nv):
+    f = nv.nvfp4_ldlq
+    wsb = nv.nvfp4_ldlq_workspace_bytes(8, 64)
+    assert wsb >= 8 * (64 * 64 + 2 * 8 * 64)
+
+    def call(dtype=1, rows=8, cols=64, block=16, H=FAKE8, sc=FAKE, S=FAKE, damp=0.01, q=FAKE,
+             st=FAKE, ws=P(0x200000), wsb=wsb):
+        return f(FAKE, dtype, rows, cols, block, H, sc, S, ctypes.c_double(damp), q, st, ws, wsb,
+                 None)
+
+    assert call(dtype=3) == -4
+    assert call(block=24) == -3
+    assert call(cols=48) == -2                   # columns in tiles of 64
+    assert call(damp=-1.0) == -5
+    assert call(damp=float("nan")) == -5
+    assert call(st=None) == -1
+    assert call(S=None) == -1
+    assert call(H=None) == -1
+    assert call(H=P(0x100004)) == -7
+    assert call(wsb=wsb - 1) == -6
+    assert call(ws=P(0x200010)) == -7
