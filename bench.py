@@ -51,7 +51,10 @@ def parse():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain device copy of known size (for counter scaling)")
     ap.add_argument("--no-rows", action="store_true",
-                    help="skip the window / reference-scale / online measurements")
+                    help="skip the window / reference-scale / online / GPTQ measurements")
+    ap.add_argument("--c4-layers", type=int, default=2,
+                    help="Llama-3-70B-shaped layers to stream through the WMSE quantizer "
+                         "(80 is the whole model)")
     return ap.parse_args()
 
 
@@ -132,6 +135,8 @@ def measure_rows(nv, workloads, torch, dev, layer):
         table8[str(B)] = {m: round(1e3 * _timed(torch, lambda: nv.quantize_online(
             xb, m, 0.002, 16, imp, layout="swizzled"), 20), 1)
             for m in ("absmax", "scalesweep_mse", "scalesweep_wmse")}
+    del t
+    t = workloads.online_tensors(dev)
     k2 = t["k"].reshape(-1, 128)
     ms_imp = _timed(torch, lambda: nv.channel_sq_norms(k2, t["k"].shape[2], 8, 1, 4), 5)
     out["f3_online"] = {"workload": "online tensors (activations [8192, 4096]; K, V "
@@ -139,7 +144,46 @@ def measure_rows(nv, workloads, torch, dev, layer):
                                     "swizzled scales", **onl,
                         "hidden8192_us_per_call": table8,
                         "importance_q_from_k_ms": round(ms_imp, 4)}
+    del t
+
+    # GPTQ (LDLQ) with ScaleSweep-WMSE scales fixed beforehand, q_proj and a synthetic Hessian
+    g = workloads.generator(dev, 61, 99)
+    X = torch.randn((1024, 4096), generator=g, device=dev, dtype=torch.float64) * \
+        torch.exp(0.7 * torch.randn(4096, generator=g, device=dev, dtype=torch.float64))
+    H = (X.T @ X).contiguous()
+    del X
+    imp = torch.diagonal(H).float().contiguous()
+    _, scg, Sg = nv.quantize(xq, "scalesweep_wmse", 16, weight=imp)
+    ms_gptq = _timed(torch, lambda: nv.ldlq(xq, H, scg, Sg, 16, 0.01, check=False), 3)
+    out["f4_gptq"] = {"workload": "q_proj [4096, 4096] bf16, Hessian X^T X of 1024 synthetic "
+                                  "tokens, ScaleSweep-WMSE scales, damping 0.01",
+                      "ms_per_call": round(ms_gptq, 2)}
     return out
+
+
+def measure_llama70b(nv, workloads, torch, dev, layers):
+    """Llama-3-70B-shaped layers generated on the device one at a time and quantized with
+    ScaleSweep-WMSE in one batched call each (dynamic S per tensor); generation untimed."""
+    total_ms, elems = 0.0, 0
+    for li in range(layers):
+        lay = workloads.llama70b_layer(li, dev)
+        xs = [lay[n][0] for n in lay]
+        ws_ = [lay[n][1] for n in lay]
+        outs = [(torch.empty((x.shape[0], x.shape[1] // 2), dtype=torch.uint8, device=dev),
+                 torch.empty((x.shape[0], x.shape[1] // 16), dtype=torch.uint8, device=dev),
+                 torch.empty(1, dtype=torch.float32, device=dev)) for x in xs]
+        torch.cuda.synchronize()
+        total_ms += _timed(torch, lambda: nv.quantize_batched(xs, "scalesweep_wmse", 16,
+                                                              weights=ws_, outs=outs), 1)
+        elems += sum(x.numel() for x in xs)
+        del lay, xs, ws_, outs
+        print(f"llama70b layer {li + 1}/{layers}: {total_ms:.1f} ms so far", file=sys.stderr,
+              flush=True)
+    return {"workload": "Llama-3-70B-shaped decoder layers (q/o 8192^2, k/v 1024x8192, "
+                        "gate/up 28672x8192, down 8192x28672), bf16, ScaleSweep-WMSE, block 16",
+            "layers": layers, "ms_per_layer": round(total_ms / layers, 3),
+            "input_GBps": round(2 * elems / total_ms / 1e6, 1),
+            "extrapolated_80_layers_s": round(total_ms / layers * 80 / 1e3, 2)}
 
 
 def main():
@@ -249,6 +293,8 @@ def main():
     }
 
     rows = None if args.no_rows else measure_rows(nv, workloads, torch, dev, layer)
+    if rows is not None and args.c4_layers > 0:
+        rows["c4_llama70b_streamed"] = measure_llama70b(nv, workloads, torch, dev, args.c4_layers)
 
     if args.copy_calibration:
         src = torch.empty(in_bytes // 4, dtype=torch.float32, device=dev).fill_(1.0)

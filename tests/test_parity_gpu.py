@@ -303,3 +303,25 @@ def test_batched_full_layer_sampled(nv):
                                            w.cpu().numpy())
         assert np.array_equal(sc[rows].cpu().numpy(), sc_ref)
         assert np.array_equal(q[rows].cpu().numpy(), q_ref)
+
+
+def test_parity_llama70b_layer_sampled(nv):
+    """One Llama-3-70B-shaped layer (855.6 M bf16 elements) through the batched WMSE call used
+    for streaming the model; sampled rows of every tensor against the oracle with that tensor's
+    global scale."""
+    layer = workloads.llama70b_layer(3, DEV)
+    names = list(layer)
+    xs = [layer[n][0] for n in names]
+    ws = [layer[n][1] for n in names]
+    outs = nv.quantize_batched(xs, "scalesweep_wmse", 16, weights=ws)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(70)
+    for x, w, (q, sc, S) in zip(xs, ws, outs):
+        xh = workloads.host_array(x)
+        rows = np.sort(rng.choice(x.shape[0], 2, replace=False))
+        S_ref = oracle.tensor_scale(xh, 256.0)
+        assert np.float32(S.item()) == np.float32(S_ref)
+        _, q_ref, sc_ref = oracle.quantize("scalesweep_wmse", xh[rows], 16, 256.0, S_ref,
+                                           w.cpu().numpy())
+        assert np.array_equal(sc[rows].cpu().numpy(), sc_ref)
+        assert np.array_equal(q[rows].cpu().numpy(), q_ref)
