@@ -6,13 +6,16 @@
 #include <hip/hip_runtime.h>
 
 #include <math.h>
+#include <stdint.h>
 
 namespace nvfp4_exact {
 
-// Midpoints between consecutive E2M1 magnitudes {0, 0.5, 1, 1.5, 2, 3, 4, 6}.
+// Midpoints between consecutive E2M1 magnitudes {0, 0.5, 1, 1.5, 2, 3, 4, 6}: 4 m_k is
+// 1, 3, 5, 7, 10, 14, 20 for k = 0..6, one byte each of a 64-bit constant (exact; a shift
+// and a conversion even when k is not a compile-time constant).
 __device__ __forceinline__ double e2m1_mid(int k) {
-    return k == 0 ? 0.25 : k == 1 ? 0.75 : k == 2 ? 1.25 : k == 3 ? 1.75
-         : k == 4 ? 2.5 : k == 5 ? 3.5 : 5.0;
+    const uint64_t quads = 0x00140E0A07050301ull;
+    return (double)(int)((quads >> (8 * k)) & 0xFFu) * 0.25;
 }
 
 __device__ __forceinline__ double e2m1_value(int k) {
@@ -26,18 +29,21 @@ __device__ __forceinline__ double e4m3_f64(int c) {
     return a ? ldexp(1.0 + 0.125 * b, a - 7) : ldexp(0.125 * b, -6);
 }
 
-// Index of the E2M1 value nearest to a / s (a >= 0, s > 0): the number of midpoints m_k with
-// a > m_k s, where a midpoint that a meets exactly counts only if it leads to an even code.
-// The products m_k s are rounded once in binary64 (exact when s is an E4M3 value).
+// Index of the E2M1 value nearest to a / s (a >= 0, s > 0): the number of midpoints m_j with
+// a > m_j s, where a midpoint that a meets exactly counts only if it leads to an even code.
+// The products m_j s are rounded once in binary64 (exact when s is an E4M3 value).  They
+// increase with j, so the count is found by a binary search over the seven midpoints (three
+// products instead of seven).
+__device__ __forceinline__ bool fp4_passes(double a, double s, int j) {
+    const double m = e2m1_mid(j) * s;
+    return a > m || (a == m && ((j + 1) & 1) == 0);
+}
+
 __device__ __forceinline__ int round_fp4_index(double a, double s) {
     if (s == 0.0) return 0;
-    int k = 0;
-#pragma unroll
-    for (int j = 0; j < 7; ++j) {
-        const double m = e2m1_mid(j) * s;
-        const bool up = a > m || (a == m && ((j + 1) & 1) == 0);
-        k = (k == j && up) ? j + 1 : k;
-    }
+    int k = fp4_passes(a, s, 3) ? 4 : 0;            // midpoints 0..3 all passed, or not 3
+    k += fp4_passes(a, s, k + 1) ? 2 : 0;           // then j = k+1 decides two more
+    k += fp4_passes(a, s, k) ? 1 : 0;               // and j = k one more
     return k;
 }
 

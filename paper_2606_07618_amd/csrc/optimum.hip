@@ -49,6 +49,7 @@ __device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* x, int64_t 
 template <int N>
 __device__ double block_loss_f64(const float* ys, const float* ws, bool weighted, double s) {
     double J = 0.0;
+#pragma unroll 2
     for (int i = 0; i < N; ++i) {
         const double a = fabs((double)ys[i]);
         const double g = e2m1_value(round_fp4_index(a, s));
@@ -87,6 +88,9 @@ __global__ __launch_bounds__(kWave) void optimum_kernel(const In* __restrict__ x
     constexpr int P = Pow2Breaks<N>::P;
     __shared__ double bp[P];
     __shared__ float ys[N], wsh[N];
+    __shared__ double ad[N], wd[N], wad[N];   // |y|, w, w |y| in binary64 (per block)
+    __shared__ double g_tab[8];
+    if (threadIdx.x < 8) g_tab[threadIdx.x] = e2m1_value(threadIdx.x);
     const int lane = threadIdx.x;
     const float S = tensor_scale[0];
     const bool weighted = colw != nullptr;
@@ -98,6 +102,11 @@ __global__ __launch_bounds__(kWave) void optimum_kernel(const In* __restrict__ x
             const float y = __fdiv_rn(load_elem<In>(x, blk * N + i), S);   // y = RN32(x / S)
             ys[i] = y;
             wsh[i] = weighted ? colw[kb * N + i] : 1.0f;
+            const double a = fabs((double)y);
+            const double wi = weighted ? (double)wsh[i] : 1.0;
+            ad[i] = a;
+            wd[i] = wi;
+            wad[i] = wi * a;
         }
         __syncthreads();
         for (int i = 0; i < N; i += kWave) {
@@ -116,9 +125,10 @@ __global__ __launch_bounds__(kWave) void optimum_kernel(const In* __restrict__ x
         __syncthreads();
         // ascending bitonic sort of the P breakpoints (+inf padding sorts last)
         for (int size = 2; size <= P; size <<= 1) {
-            for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int ls = __builtin_ctz(size) - 1; ls >= 0; --ls) {   // stride = 2^ls
+                const int stride = 1 << ls;
                 for (int t = lane; t < P / 2; t += kWave) {
-                    const int i = 2 * stride * (t / stride) + (t % stride);
+                    const int i = ((t >> ls) << (ls + 1)) + (t & (stride - 1));
                     const int j = i + stride;
                     const bool asc = (i & size) == 0;
                     const double u = bp[i], v = bp[j];
@@ -142,14 +152,15 @@ __global__ __launch_bounds__(kWave) void optimum_kernel(const In* __restrict__ x
             const double hi = seg == nb ? INFINITY : bp[seg];
             if (!(hi > lo)) continue;
             const double s_ref = seg == 0 ? 0.5 * hi : seg == nb ? 2.0 * lo : 0.5 * (lo + hi);
-            double A = 0.0, B = 0.0, C = 0.0;
+            // A = sum w y^2 is the same on every piece (and equals A0 bit for bit: w |y| |y|
+            // and w y y round alike), so only B and C are summed here
+            const double A = A0;
+            double B = 0.0, C = 0.0;
+#pragma unroll 4
             for (int i = 0; i < N; ++i) {
-                const double a = fabs((double)ys[i]);
-                const double wi = weighted ? (double)wsh[i] : 1.0;
-                const double g = e2m1_value(round_fp4_index(a, s_ref));
-                A += wi * a * a;
-                B += wi * a * g;
-                C += wi * g * g;
+                const double g = g_tab[round_fp4_index(ad[i], s_ref)];
+                B += wad[i] * g;                 // (w |y|) g, as w * a * g associates
+                C += wd[i] * g * g;
             }
             Best cand{0.0, 0.0, seg};
             if (C <= 0.0) {
