@@ -61,7 +61,7 @@ typedef enum {
     NVFP4_ERR_HIP = -8        /* a kernel launch failed */
 } nvfp4_status;
 
-/* Bytes of device workspace the dynamic-scale path needs (a small constant, about 1 KiB).
+/* Bytes of device workspace the dynamic-scale path needs (a small constant, 10 KiB).
  * It carries the per-workgroup |x| maxima of the reduction kernel and the resulting S and 1/S
  * to the quantization kernel of the same call; it needs no initialization and holds nothing
  * between calls.  Static-scale calls do not touch it (it may be NULL). */
@@ -244,18 +244,16 @@ size_t nvfp4_batched_workspace_bytes(int count);
  * 3 ScaleSweep-WMSE), each with its own dynamic global scale: the per-tensor round-to-nearest
  * pipeline of the experiment setup applied to, e.g., the weights of one decoder layer.  Every
  * tensor's outputs are bit-identical to its single-tensor call.  `tensors` is a host array;
- * the descriptors may be reused once the call returns.  The |x| reductions run on
- * `side_stream` and the quantization kernels on `stream`, ordered by events: the largest
- * tensor is reduced and quantized first, and the other tensors' bandwidth-bound reductions
- * overlap its arithmetic-bound sweep; side_stream == NULL or == stream runs everything on
- * `stream`.  Both streams must be of
- * default priority.  On return the work of both streams is ordered before any later work
- * enqueued on `stream`.  workspace: >= nvfp4_batched_workspace_bytes(count), 16-byte
- * aligned, no initialization.  Errors as for the single-tensor calls (validated for every
- * tensor before any launch); count < 0 or an unknown method: NVFP4_ERR_ARG. */
+ * the descriptors may be reused once the call returns.  Everything runs on `stream`: the
+ * smallest non-empty tensor's |x| reduction first, then one quantization kernel per tensor in
+ * ascending size, each of which also reduces max |x| of the next tensor (atomic maxima into
+ * that tensor's workspace), so that only the smallest reduction is not overlapped with a
+ * sweep.  workspace: >= nvfp4_batched_workspace_bytes(count), 16-byte aligned, no
+ * initialization; two calls in flight at the same time must not share it.  Errors as for the
+ * single-tensor calls (validated for every tensor before any launch); count < 0 or an unknown
+ * method: NVFP4_ERR_ARG. */
 int nvfp4_quant_batched(int method, const nvfp4_tensor* tensors, int count, int dtype, int block,
-                        float fp8_range, void* workspace, size_t workspace_bytes, void* stream,
-                        void* side_stream);
+                        float fp8_range, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Reconstruction x_hat_i = q_i * s_{block(i)} * S (NVFP4 Quantization section) into out
  * [rows, cols] binary32 (out_dtype must be NVFP4_IN_F32): q * s is exact, so each output is the

@@ -49,10 +49,15 @@ constexpr int kLaneElems = 16;
 enum Method { kAbsMax = 0, kFourSix = 1, kSweepMse = 2, kSweepWmse = 3, kWindowMse = 4, kWindowWmse = 5 };
 
 // Workspace words: one |x|-maximum bit pattern per workgroup of the reduction pass, then S
-// and 1/S.
+// and 1/S; from word kSlotWord0 on, 64 |x|-maximum slots, each on its own 128-byte line,
+// which the workgroups of the quantization kernel of the preceding tensor of a batched call
+// raise atomically (slot = workgroup index mod 64).  Atomics on one line serialize (about
+// 11 ns apiece measured on MI355X, i.e. 160 us for one per workgroup of a 14336-workgroup
+// grid); spread over 64 lines they cost nothing measurable.
 constexpr int kMaxPartials = 256;
 constexpr int kWsScale = kMaxPartials, kWsRecip = kMaxPartials + 1;
-constexpr size_t kWorkspaceBytes = (kMaxPartials + 4) * sizeof(uint32_t);
+constexpr int kSlotWord0 = 512, kSlotStride = 32, kSlots = 64;
+constexpr size_t kWorkspaceBytes = (kSlotWord0 + kSlots * kSlotStride) * sizeof(uint32_t);
 
 
 // Candidate band for the exact re-scoring (relative, plus an absolute floor for losses that
@@ -366,8 +371,14 @@ __global__ __launch_bounds__(kThreads) void amax_kernel(const In* __restrict__ x
 
 // Folds the per-workgroup maxima into S and 1/S (one wave): S goes to the caller's output
 // and, with 1/S, to the workspace words after the partials, for the quantization kernel.
+// With zero_count > 0 it also clears the |x|-maximum slots of zero_count workspaces laid out
+// zero_stride words apart from zero_base (the other tensors of a batched call).
 __global__ __launch_bounds__(64) void scale_kernel(uint32_t* __restrict__ ws, int npart,
-                                                   float denom, float* __restrict__ tensor_scale) {
+                                                   float denom, float* __restrict__ tensor_scale,
+                                                   uint32_t* __restrict__ zero_base, int zero_count,
+                                                   int64_t zero_stride) {
+    for (int t = threadIdx.x; t < zero_count * kSlots; t += 64)
+        zero_base[(t / kSlots) * zero_stride + kSlotWord0 + (t % kSlots) * kSlotStride] = 0u;
     uint32_t m = 0;
     for (int i = threadIdx.x; i < npart; i += 64) m = max(m, ws[i]);
 #pragma unroll
@@ -386,15 +397,29 @@ __global__ void write_scale_kernel(float* tensor_scale, float S) { tensor_scale[
 // Quantization kernel.
 // ---------------------------------------------------------------------------------------
 
+// Source of the global scale in the quantization kernel.
+enum ScaleSource {
+    kScaleStatic = 0,         // Params::S, Params::rS (given by the caller)
+    kScaleWorkspace = 1,      // S and 1/S formed by scale_kernel earlier on the stream
+    kScaleSlots = 2,          // the maximum of the workspace's |x| slots (raised atomically by
+                              // the preceding kernel of a batched call), folded here
+};
+
 struct Params {
     int64_t nblocks;          // micro-blocks in the tensor
     uint32_t bpr;             // micro-blocks per row
     uint32_t bpr_magic;       // blk / bpr = (umulhi(blk, magic) + ((blk - hi) >> 1)) >> (shift - 1)
     uint32_t bpr_shift;
-    int dynamic;              // S, 1/S from the workspace (else given)
+    int scale_src;            // where S comes from (ScaleSource)
     float S, rS;              // static global scale and its reciprocal
+    float denom;              // 6 D, for kScaleSlots
     const uint32_t* ws;       // workspace of the dynamic path
-    float* tensor_scale;      // static path: written once, by the first lane of the grid
+    float* tensor_scale;      // static and slot paths: written once, by the first lane of the grid
+    const uint4* nx;          // batched calls: the next tensor, whose |x| maximum the first
+    int64_t nx_vec;           //   nx_wgs workgroups of the grid reduce into nx_slots (nx_vec
+    int64_t nx_per;           //   16-byte vectors, nx_per per workgroup); nx_wgs = 0: none
+    uint32_t* nx_slots;
+    uint32_t nx_wgs;
     int win_tight;            // window variants: per-mantissa offsets (else win_lo..win_hi)
     int win_lo, win_hi;
     int swizzled;             // scales in 128 x 4 tiles (else row-major)
@@ -513,6 +538,39 @@ __device__ int choose_window(const float (&y)[kLaneElems], const float (&w)[kLan
     return dstar < ncand ? lo + dstar : lo;   // dstar >= ncand only if every loss is NaN
 }
 
+// Batched calls: a reducer workgroup of the quantization grid streams its share of the next
+// tensor (16 vectors of 16 bytes in flight per lane) and raises slot blockIdx mod 64 of that
+// tensor's workspace with one relaxed device-scope atomic maximum; the next kernel on the
+// stream folds the slots after this grid has completed.  The reducers are the first
+// workgroups of the grid, so they are dispatched first and stream while the other
+// workgroups of the grid run the arithmetic-bound sweep beside them.
+template <typename In>
+__device__ void reduce_share(const Params& p) {
+    const int64_t b0 = (int64_t)blockIdx.x * p.nx_per;
+    const int64_t b1 = min(b0 + p.nx_per, p.nx_vec);
+    uint32_t m = 0;
+    int64_t i = b0 + threadIdx.x;
+    for (; i + 15 * kThreads < b1; i += 16 * kThreads) {
+        uint4 d[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) d[k] = p.nx[i + k * kThreads];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) m = max(m, absmax_bits(d[k], In()));
+    }
+    for (; i < b1; i += kThreads) m = max(m, absmax_bits(p.nx[i], In()));
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off, 64));
+    __shared__ uint32_t s_red[kThreads / 64];
+    if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        m = max(max(s_red[0], s_red[1]), max(s_red[2], s_red[3]));
+        if (m != 0u)
+            __hip_atomic_fetch_max(p.nx_slots + (blockIdx.x & (kSlots - 1)) * kSlotStride, m,
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
 template <int METHOD, typename In, int N>
 __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ x,
                                                          const float* __restrict__ colw,
@@ -522,8 +580,13 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
     constexpr bool WEIGHTED_OBJ = METHOD == kSweepWmse || METHOD == kFourSix || METHOD == kWindowWmse;
     __shared__ Scale tab_all[kTabSize];
     Scale* tab = tab_all + kTabLo;                 // tab[c] for codes c in -16..143
+    if (blockIdx.x < p.nx_wgs) {        // uniform per workgroup
+        reduce_share<In>(p);
+        return;
+    }
+    const uint32_t tile = blockIdx.x - p.nx_wgs;      // the workgroup's tile of this tensor
     const int lane = threadIdx.x & 63;
-    const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t gtid = (int64_t)tile * kThreads + threadIdx.x;
     const int64_t blk = gtid / LPB;
     const int part = (int)(gtid % LPB);
     const int group_base = lane - part;
@@ -549,15 +612,32 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
         for (int i = 0; i < kLaneElems; ++i) w[i] = 1.0f;
     }
     fill_scale_table<METHOD == kAbsMax || METHOD == kFourSix>(tab_all);
+    __shared__ float s_scale[2];
+    if (p.scale_src == kScaleSlots && threadIdx.x < 64) {
+        // the slots were raised by the previous kernel on the stream: wave 0 folds them
+        uint32_t m = p.ws[kSlotWord0 + threadIdx.x * kSlotStride];
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off, 64));
+        if (threadIdx.x == 0) {
+            const float Sg = global_scale(m, p.denom);
+            s_scale[0] = Sg;
+            s_scale[1] = __fdiv_rn(1.0f, Sg);
+        }
+    }
     __syncthreads();
     float S, rS;
-    if (p.dynamic) {      // formed by scale_kernel, earlier on the same stream
+    if (p.scale_src == kScaleWorkspace) {      // formed by scale_kernel, earlier on the stream
         S = __uint_as_float(p.ws[kWsScale]);
         rS = __uint_as_float(p.ws[kWsRecip]);
     } else {
-        S = p.S;
-        rS = p.rS;
-        if (blockIdx.x == 0 && threadIdx.x == 0 && p.tensor_scale) p.tensor_scale[0] = S;
+        if (p.scale_src == kScaleSlots) {
+            S = s_scale[0];
+            rS = s_scale[1];
+        } else {
+            S = p.S;
+            rS = p.rS;
+        }
+        if (tile == 0 && threadIdx.x == 0 && p.tensor_scale) p.tensor_scale[0] = S;
     }
     const bool fast_div = S >= 0x1p-26f && S <= 0x1p26f;
 
@@ -808,11 +888,22 @@ struct Call {
     int64_t wgroups = 1, wgroup_rows = 1;
 };
 
+// Workgroups of the quantization kernel: one lane per 16 elements, one workgroup per tile.
+int64_t quant_grid(const Call& c) {
+    const int64_t lanes = c.rows * c.cols / kLaneElems;
+    return (lanes + kThreads - 1) / kThreads;
+}
+
+// Reducer workgroups for a next tensor of nvec 16-byte vectors: one per 64 KiB, at most one
+// per CU (each keeps 64 KiB in flight, so 256 of them saturate HBM).
+int64_t reducer_wgs(int64_t nvec) {
+    const int64_t r = (nvec + 4095) / 4096;
+    return r < 256 ? r : 256;
+}
+
 template <int METHOD, typename In, int N>
 hipError_t launch_quant(const Call& c, const Params& p) {
-    constexpr int LPB = N / kLaneElems;
-    const int64_t lanes = p.nblocks * LPB;
-    const int64_t grid = (lanes + kThreads - 1) / kThreads;   // one workgroup per tile
+    const int64_t grid = quant_grid(c) + p.nx_wgs;              // reducers, then one per tile
     hipLaunchKernelGGL((quant_kernel<METHOD, In, N>), dim3((unsigned)grid), dim3(kThreads), 0, c.stream,
                        static_cast<const In*>(c.x), c.colw, c.q, c.scales, p);
     return hipGetLastError();
@@ -863,8 +954,10 @@ int validate(const Call& c) {
     return NVFP4_OK;
 }
 
-// Dynamic global scale of a non-empty tensor: the |x| reduction and the fold into S, 1/S.
-hipError_t launch_scale(const Call& c, hipStream_t stream, int* npart) {
+// Dynamic global scale of a non-empty tensor: the |x| reduction and the fold into S, 1/S
+// (which also clears the |x| slots of zero_count workspaces from zero_base, for a batched call).
+hipError_t launch_scale(const Call& c, hipStream_t stream, int* npart, void* zero_base = nullptr,
+                        int zero_count = 0) {
     const int64_t n = c.rows * c.cols;
     const int64_t nvec = n * (c.dtype == NVFP4_IN_F32 ? 4 : 2) / 16;
     int64_t g = (nvec + kThreads * 8 - 1) / (kThreads * 8);
@@ -880,22 +973,40 @@ hipError_t launch_scale(const Call& c, hipStream_t stream, int* npart) {
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(scale_kernel, dim3(1), dim3(64), 0, stream, static_cast<uint32_t*>(c.ws),
-                       (int)g, 6.0f * c.fp8_range, c.tensor_scale);
+                       (int)g, 6.0f * c.fp8_range, c.tensor_scale, static_cast<uint32_t*>(zero_base),
+                       zero_count, (int64_t)(kWorkspaceBytes / sizeof(uint32_t)));
     return hipGetLastError();
 }
 
-// The quantization kernel of a non-empty tensor (after launch_scale for a dynamic scale).
-hipError_t launch_main(const Call& c, hipStream_t stream) {
+// What a quantization kernel of a batched call does beyond its own tensor: where its S comes
+// from, and the next tensor whose |x| maximum it reduces (nullptr: none).
+struct Chain {
+    int scale_src = kScaleWorkspace;
+    const void* nx = nullptr;
+    int64_t nx_bytes = 0;
+    uint32_t* nx_ws = nullptr;
+};
+
+
+// The quantization kernel of a non-empty tensor (after launch_scale for a dynamic scale, or
+// after the kernel that raised its |x| slots in a batched call).
+hipError_t launch_main(const Call& c, hipStream_t stream, const Chain& chain = Chain()) {
     const bool dynamic = c.static_scale == 0.0f;
     Params p;
     p.nblocks = c.rows * c.cols / c.block;
     p.bpr = (uint32_t)(c.cols / c.block);
     make_divider(p.bpr, &p.bpr_magic, &p.bpr_shift);
-    p.dynamic = dynamic ? 1 : 0;
+    p.scale_src = dynamic ? chain.scale_src : kScaleStatic;
     p.S = dynamic ? 0.0f : c.static_scale;
     p.rS = dynamic ? 0.0f : 1.0f / c.static_scale;
+    p.denom = 6.0f * c.fp8_range;
     p.ws = static_cast<const uint32_t*>(c.ws);
     p.tensor_scale = c.tensor_scale;
+    p.nx = static_cast<const uint4*>(chain.nx);
+    p.nx_vec = chain.nx ? chain.nx_bytes / 16 : 0;
+    p.nx_wgs = (uint32_t)reducer_wgs(p.nx_vec);
+    p.nx_per = p.nx_wgs ? (p.nx_vec + p.nx_wgs - 1) / p.nx_wgs : 0;
+    p.nx_slots = chain.nx_ws ? chain.nx_ws + kSlotWord0 : nullptr;
     p.swizzled = c.layout == NVFP4_SCALES_SWIZZLED ? 1 : 0;
     p.sw_kt = (uint32_t)((c.cols / c.block + 3) / 4);
     p.wgroups = (uint32_t)c.wgroups;
@@ -932,63 +1043,62 @@ int run_quant(const Call& c) {
     return launch_main(c, c.stream) == hipSuccess ? NVFP4_OK : NVFP4_ERR_HIP;
 }
 
-// Several tensors, dynamic scales.  The largest tensor goes first: its reduction, then (main
-// stream) its quantization kernel; meanwhile the side stream reduces all the other tensors,
-// and the main stream waits once for that before quantizing them back to back.  So the
-// bandwidth-bound reductions overlap the arithmetic-bound sweep of the largest tensor, and
-// the main stream carries two event waits in all (each wait costs a few microseconds even
-// when its event has long completed).
+// Several tensors, dynamic scales, one stream.  The non-empty tensors form a chain in
+// ascending size: the first is reduced by amax_kernel and folded by scale_kernel (which also
+// clears every tensor's |x| slots); each quantization kernel then also reduces the next
+// tensor of the chain into that tensor's slots, and the next kernel folds them into its S.
+// So every reduction but the smallest tensor's rides along with an arithmetic-bound sweep,
+// and no kernel sits between two sweeps.  Ascending order keeps the next tensor's share per
+// workgroup small (at most 4x its own tile for a decoder layer).
 int run_batched(int method, const nvfp4_tensor* t, int count, int dtype, int block,
-                float fp8_range, void* ws, size_t ws_bytes, hipStream_t main, hipStream_t side) {
+                float fp8_range, void* ws, size_t ws_bytes, hipStream_t main) {
     if (count < 0) return NVFP4_ERR_ARG;
     if (count > 0 && !t) return NVFP4_ERR_NULL;
     if (method < kAbsMax || method > kSweepWmse) return NVFP4_ERR_ARG;
     if (count > 0 && (!ws || ws_bytes < (size_t)count * kWorkspaceBytes)) return NVFP4_ERR_WORKSPACE;
     if (count > 0 && !aligned(ws, 16)) return NVFP4_ERR_ALIGN;
+    auto ws_of = [&](int k) { return static_cast<char*>(ws) + (size_t)k * kWorkspaceBytes; };
     auto call_of = [&](int k) {
         return Call{method, t[k].x, dtype, t[k].rows, t[k].cols, block, t[k].col_weight,
                     fp8_range, 0.0f, t[k].tensor_scale, t[k].q, t[k].scales,
-                    static_cast<char*>(ws) + (size_t)k * kWorkspaceBytes, kWorkspaceBytes, main};
+                    ws_of(k), kWorkspaceBytes, main};
     };
-    int first = -1;
-    int64_t first_n = -1;
+    int order[256];
+    int* chain = count <= 256 ? order : new int[count];
+    int len = 0;
     for (int k = 0; k < count; ++k) {
         const int rc = validate(call_of(k));
-        if (rc != NVFP4_OK) return rc;
-        if (t[k].rows * t[k].cols > first_n) {
-            first_n = t[k].rows * t[k].cols;
-            first = k;
+        if (rc != NVFP4_OK) {
+            if (chain != order) delete[] chain;
+            return rc;
         }
+        if (t[k].rows * t[k].cols > 0) chain[len++] = k;
     }
-    if (count == 0) return NVFP4_OK;
-    if (side == main) side = nullptr;
-    hipStream_t red = side ? side : main;
-    hipEvent_t ev[3] = {nullptr, nullptr, nullptr};   // main ready, first reduced, rest reduced
+    auto size_of = [&](int k) { return t[k].rows * t[k].cols; };
+    for (int a = 1; a < len; ++a) {          // stable insertion sort by size
+        const int k = chain[a];
+        int b = a;
+        for (; b > 0 && size_of(chain[b - 1]) > size_of(k); --b) chain[b] = chain[b - 1];
+        chain[b] = k;
+    }
+    const int64_t elem_bytes = dtype == NVFP4_IN_F32 ? 4 : 2;
     bool ok = true;
-    if (side) {
-        for (int e = 0; ok && e < 3; ++e) ok = hipEventCreateWithFlags(&ev[e], hipEventDisableTiming) == hipSuccess;
-        // the reductions start after the work already queued on the main stream
-        ok = ok && hipEventRecord(ev[0], main) == hipSuccess && hipStreamWaitEvent(side, ev[0], 0) == hipSuccess;
-    }
+    for (int k = 0; ok && k < count; ++k)
+        if (size_of(k) == 0) ok = launch_empty(call_of(k), main) == hipSuccess;
     int npart = 0;
-    const Call cf = call_of(first);
-    if (ok && first_n > 0) ok = launch_scale(cf, red, &npart) == hipSuccess;
-    if (ok && side) ok = hipEventRecord(ev[1], side) == hipSuccess && hipStreamWaitEvent(main, ev[1], 0) == hipSuccess;
-    if (ok) ok = (first_n > 0 ? launch_main(cf, main) : launch_empty(cf, main)) == hipSuccess;
-    bool any_rest = false;
-    for (int k = 0; ok && k < count; ++k) {
-        if (k == first || t[k].rows * t[k].cols == 0) continue;
-        ok = launch_scale(call_of(k), red, &npart) == hipSuccess;
-        any_rest = true;
+    if (ok && len > 0) ok = launch_scale(call_of(chain[0]), main, &npart, ws, count) == hipSuccess;
+    for (int j = 0; ok && j < len; ++j) {
+        Chain ch;
+        ch.scale_src = j == 0 ? kScaleWorkspace : kScaleSlots;
+        if (j + 1 < len) {
+            const int kn = chain[j + 1];
+            ch.nx = t[kn].x;
+            ch.nx_bytes = size_of(kn) * elem_bytes;
+            ch.nx_ws = reinterpret_cast<uint32_t*>(ws_of(kn));
+        }
+        ok = launch_main(call_of(chain[j]), main, ch) == hipSuccess;
     }
-    if (ok && side && any_rest) ok = hipEventRecord(ev[2], side) == hipSuccess && hipStreamWaitEvent(main, ev[2], 0) == hipSuccess;
-    for (int k = 0; ok && k < count; ++k) {
-        if (k == first) continue;
-        const Call c = call_of(k);
-        ok = (c.rows * c.cols > 0 ? launch_main(c, main) : launch_empty(c, main)) == hipSuccess;
-    }
-    for (int e = 0; e < 3; ++e)      // events may be destroyed while pending
-        if (ev[e]) hipEventDestroy(ev[e]);
+    if (chain != order) delete[] chain;
     return ok ? NVFP4_OK : NVFP4_ERR_HIP;
 }
 
@@ -1065,10 +1175,9 @@ size_t nvfp4_batched_workspace_bytes(int count) {
 }
 
 int nvfp4_quant_batched(int method, const nvfp4_tensor* tensors, int count, int dtype, int block,
-                        float fp8_range, void* workspace, size_t workspace_bytes, void* stream,
-                        void* side_stream) {
+                        float fp8_range, void* workspace, size_t workspace_bytes, void* stream) {
     return run_batched(method, tensors, count, dtype, block, fp8_range, workspace,
-                       workspace_bytes, (hipStream_t)stream, (hipStream_t)side_stream);
+                       workspace_bytes, (hipStream_t)stream);
 }
 
 const char* nvfp4_status_string(int status) {

@@ -36,7 +36,7 @@ def _load():
     sigs = {
         "nvfp4_workspace_bytes": (SZ, []),
         "nvfp4_batched_workspace_bytes": (SZ, [I]),
-        "nvfp4_quant_batched": (I, [I, P, I, I, I, F, P, SZ, P, P]),
+        "nvfp4_quant_batched": (I, [I, P, I, I, I, F, P, SZ, P]),
         "nvfp4_status_string": (ctypes.c_char_p, [I]),
         "nvfp4_quant_absmax": (I, quant),
         "nvfp4_quant_four_over_six": (I, quant_w),
@@ -209,20 +209,9 @@ def quantize_window(x: torch.Tensor, block: int = 16, weight: torch.Tensor | Non
     return q, sc, S
 
 
-_side_streams = {}
-
-
-def side_stream(device) -> torch.cuda.Stream:
-    """A default-priority stream per device for the batched call's reductions."""
-    key = torch.device(device).index or 0
-    if key not in _side_streams:
-        _side_streams[key] = torch.cuda.Stream(device=device)
-    return _side_streams[key]
-
-
 def quantize_batched(xs, method: str = "scalesweep_wmse", block: int = 16, weights=None,
                      fp8_range: float | None = None, ws: torch.Tensor | None = None,
-                     outs=None, overlap: bool = True):
+                     outs=None):
     """Quantize a list of 2-D device tensors (one dtype) with one method and a dynamic global
     scale each, in one batched call.  Returns a list of (q, scales, S)."""
     if not xs:
@@ -245,13 +234,8 @@ def quantize_batched(xs, method: str = "scalesweep_wmse", block: int = 16, weigh
     nbytes = nvfp4_batched_workspace_bytes(len(xs))
     if ws is None or ws.numel() * ws.element_size() < nbytes:
         ws = torch.empty(nbytes // 4, dtype=torch.int32, device=dev)
-    main = torch.cuda.current_stream(dev)
-    side = side_stream(dev) if overlap else main
-    if side is not main:
-        ws.record_stream(side)          # the reductions on the side stream write it
     rc = nvfp4_quant_batched(METHOD_IDS[method], ctypes.cast(arr, ctypes.c_void_p), len(xs), dt,
-                             block, ctypes.c_float(D), _ptr(ws), nbytes,
-                             ctypes.c_void_p(main.cuda_stream), ctypes.c_void_p(side.cuda_stream))
+                             block, ctypes.c_float(D), _ptr(ws), nbytes, _stream(dev))
     if rc != 0:
         raise NVFP4Error(rc, "nvfp4_quant_batched")
     return outs

@@ -121,18 +121,18 @@ def test_batched_validation(nv):
     f = nv.nvfp4_quant_batched
     ws, wsb = FAKE, nv.nvfp4_batched_workspace_bytes(2)
     a = ctypes.cast(arr, ctypes.c_void_p)
-    assert f(3, a, -1, 1, 16, ctypes.c_float(256.0), ws, wsb, None, None) == -5
-    assert f(9, a, 2, 1, 16, ctypes.c_float(256.0), ws, wsb, None, None) == -5
-    assert f(3, None, 2, 1, 16, ctypes.c_float(256.0), ws, wsb, None, None) == -1
-    assert f(3, a, 2, 1, 16, ctypes.c_float(256.0), ws, wsb - 16, None, None) == -6
-    assert f(3, a, 2, 1, 24, ctypes.c_float(256.0), ws, wsb, None, None) == -3
-    assert f(3, a, 2, 7, 16, ctypes.c_float(256.0), ws, wsb, None, None) == -4
+    assert f(3, a, -1, 1, 16, ctypes.c_float(256.0), ws, wsb, None) == -5
+    assert f(9, a, 2, 1, 16, ctypes.c_float(256.0), ws, wsb, None) == -5
+    assert f(3, None, 2, 1, 16, ctypes.c_float(256.0), ws, wsb, None) == -1
+    assert f(3, a, 2, 1, 16, ctypes.c_float(256.0), ws, wsb - 16, None) == -6
+    assert f(3, a, 2, 1, 24, ctypes.c_float(256.0), ws, wsb, None) == -3
+    assert f(3, a, 2, 7, 16, ctypes.c_float(256.0), ws, wsb, None) == -4
     arr[1].cols = 60
-    assert f(3, a, 2, 1, 16, ctypes.c_float(256.0), ws, wsb, None, None) == -2
+    assert f(3, a, 2, 1, 16, ctypes.c_float(256.0), ws, wsb, None) == -2
     arr[1].cols = 64
     arr[1].col_weight = None
-    assert f(3, a, 2, 1, 16, ctypes.c_float(256.0), ws, wsb, None, None) == -1
-    assert f(3, a, 0, 1, 16, ctypes.c_float(256.0), None, 0, None, None) == 0
+    assert f(3, a, 2, 1, 16, ctypes.c_float(256.0), ws, wsb, None) == -1
+    assert f(3, a, 0, 1, 16, ctypes.c_float(256.0), None, 0, None) == 0
 
 
 def test_window_validation(nv):

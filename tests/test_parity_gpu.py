@@ -260,32 +260,89 @@ def test_parity_online_sampled(nv):
 
 
 # ---------------------------------------------------------------------------------------
-# Batched call: the same outputs as the single-tensor calls, reductions overlapped on a side
-# stream.
+# Batched call: the same outputs as the single-tensor calls.  The call chains the tensors in
+# ascending size, each quantization kernel reducing max |x| of the next one into atomic
+# slots; the cases vary the order of sizes, ties of sizes, zero / non-finite tensors, more
+# than 256 tensors and workspace reuse.
 # ---------------------------------------------------------------------------------------
 
-@pytest.mark.parametrize("method", METHODS)
-@pytest.mark.parametrize("overlap", [True, False])
-def test_batched_matches_single_calls(nv, method, overlap):
-    g = workloads.generator(DEV, 8, 8)
-    shapes = [(512, 1024), (0, 64), (64, 4096), (1024, 512), (8, 64)]
+BATCH_SHAPES = {
+    "mixed": [(512, 1024), (0, 64), (64, 4096), (1024, 512), (8, 64)],
+    "descending": [(2048, 1024), (1024, 1024), (256, 512), (64, 128), (1, 16)],
+    "equal_sizes": [(256, 256), (128, 512), (512, 128), (256, 256), (64, 1024)],
+    "small_then_large": [(1, 16), (4096, 2048)],
+}
+
+
+def _batch_inputs(shapes, seed):
+    g = workloads.generator(DEV, 8, seed)
     xs = [workloads.llm_weight(r, c, g, DEV) if r else torch.zeros(0, c, device=DEV,
           dtype=torch.bfloat16) for r, c in shapes]
     ws = [workloads.column_importance(c, g, DEV, tokens=64) for _, c in shapes]
+    return xs, ws
+
+
+def _assert_batched_equals_single(nv, method, xs, ws, outs):
     use_w = method in ("scalesweep_wmse", "four_over_six")
-    outs = nv.quantize_batched(xs, method, 16, weights=ws if use_w else None, overlap=overlap)
     for k, x in enumerate(xs):
         q1, sc1, S1 = nv.quantize(x, method, 16, weight=ws[k] if use_w else None)
         torch.cuda.synchronize()
         q2, sc2, S2 = outs[k]
-        assert torch.equal(S1, S2) and torch.equal(sc1, sc2) and torch.equal(q1, q2), (k, shapes[k])
-    # one tensor against the oracle as well
-    check_x, check_w = xs[2], ws[2].cpu().numpy() if use_w else None
-    S_ref, q_ref, sc_ref = oracle.quantize(method, workloads.host_array(check_x), 16,
+        assert torch.equal(S1, S2) or (torch.isnan(S1).all() and torch.isnan(S2).all()), k
+        if not torch.isnan(S1).any():
+            assert torch.equal(sc1, sc2) and torch.equal(q1, q2), (k, tuple(x.shape))
+
+
+@pytest.mark.parametrize("method", METHODS)
+@pytest.mark.parametrize("case", list(BATCH_SHAPES))
+def test_batched_matches_single_calls(nv, method, case):
+    shapes = BATCH_SHAPES[case]
+    xs, ws = _batch_inputs(shapes, 8)
+    use_w = method in ("scalesweep_wmse", "four_over_six")
+    outs = nv.quantize_batched(xs, method, 16, weights=ws if use_w else None)
+    _assert_batched_equals_single(nv, method, xs, ws, outs)
+    # the largest tensor against the oracle as well
+    big = max(range(len(xs)), key=lambda k: xs[k].numel())
+    check_w = ws[big].cpu().numpy() if use_w else None
+    S_ref, q_ref, sc_ref = oracle.quantize(method, workloads.host_array(xs[big]), 16,
                                            RANGE[method], 0.0, check_w)
-    assert outs[2][2].item() == S_ref
-    assert np.array_equal(outs[2][1].cpu().numpy(), sc_ref)
-    assert np.array_equal(outs[2][0].cpu().numpy(), q_ref)
+    assert outs[big][2].item() == S_ref
+    assert np.array_equal(outs[big][1].cpu().numpy(), sc_ref)
+    assert np.array_equal(outs[big][0].cpu().numpy(), q_ref)
+
+
+@pytest.mark.parametrize("method", ["absmax", "scalesweep_mse", "scalesweep_wmse"])
+def test_batched_zero_and_nonfinite_tensors(nv, method):
+    xs, ws = _batch_inputs([(64, 256), (128, 256), (32, 512), (256, 128), (16, 64)], 9)
+    xs[1] = torch.zeros_like(xs[1])                     # S = 1
+    xs[2] = xs[2].clone()
+    xs[2][3, 17] = float("nan")                         # S = NaN (chain neighbour of others)
+    xs[4] = -xs[4].abs()                                # all negative
+    outs = nv.quantize_batched(xs, method, 16, weights=ws if method.endswith("wmse") else None)
+    torch.cuda.synchronize()
+    assert outs[1][2].item() == 1.0
+    assert np.isnan(outs[2][2].item())
+    _assert_batched_equals_single(nv, method, xs, ws, outs)
+
+
+def test_batched_many_tensors(nv):
+    """More tensors than the host's fixed chain array holds (the heap path)."""
+    g = workloads.generator(DEV, 10, 10)
+    xs = [workloads.llm_weight(2 + (k % 5), 64, g, DEV) * (1 + k % 7) for k in range(300)]
+    outs = nv.quantize_batched(xs, "scalesweep_mse", 16)
+    _assert_batched_equals_single(nv, "scalesweep_mse", xs, [None] * len(xs), outs)
+
+
+def test_batched_workspace_reuse(nv):
+    """A second call on the same workspace with smaller maxima: the slots are cleared by the
+    call itself, so the previous call's maxima never leak into S."""
+    xs, ws = _batch_inputs([(64, 512), (256, 512), (128, 1024)], 11)
+    bws = torch.full((nv.nvfp4_batched_workspace_bytes(3) // 4,), -1, dtype=torch.int32,
+                     device=DEV)                         # garbage, incl. large slot values
+    for scale in (100.0, 0.01):
+        xk = [x * scale for x in xs]
+        outs = nv.quantize_batched(xk, "scalesweep_wmse", 16, weights=ws, ws=bws)
+        _assert_batched_equals_single(nv, "scalesweep_wmse", xk, ws, outs)
 
 
 def test_batched_full_layer_sampled(nv):
