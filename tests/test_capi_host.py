@@ -80,7 +80,7 @@ def test_validation_errors(nv, name):
     assert call(nv, name, static=float("nan")) == -5
     assert call(nv, name) == -6                            # dynamic scale without workspace
     assert call(nv, name, ws=FAKE, wsb=8) == -6            # workspace too small
-    assert call(nv, name, ws=P(0x100004), wsb=4096) == -7  # misaligned workspace
+    assert call(nv, name, ws=P(0x100004), wsb=nv.nvfp4_workspace_bytes()) == -7  # misaligned
     assert call(nv, name, x=P(0x100004), **st) == -7       # misaligned x
     assert call(nv, name, q=P(0x100004), **st) == -7       # misaligned q
     if name == "nvfp4_quant_scalesweep_wmse":
