@@ -3,8 +3,8 @@
 
 One step quantizes every weight of a Llama-3-8B-shaped decoder layer (bfloat16, block 16,
 dynamic global scale with D = 256) with ScaleSweep under both objectives, MSE and WMSE: one
-batched call per objective over the layer's 7 tensors (each tensor's |x| reduction streamed
-by reducer workgroups of the previous tensor's quantization grid).  `value` is the bfloat16 input consumed
+batched call per objective over the layer's 7 tensors (each tensor's |x| reduction spread over
+the workgroups of the previous tensor's quantization grid).  `value` is the bfloat16 input consumed
 per second (both objectives read the layer).  The line also carries:
   * per-method GB/s of the same GPU's AbsMax (D = 448), 4/6 and each ScaleSweep objective,
     batched over the layer and as 7 single-tensor calls, and the time relative to AbsMax;

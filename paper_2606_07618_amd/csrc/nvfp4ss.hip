@@ -277,6 +277,63 @@ __device__ __forceinline__ float cand_loss(const float (&u)[kLaneElems], const f
     return acc0 + acc1;
 }
 
+// Losses of the window candidates d, d + 8, d + 16 (those below NC), normal codes only: the
+// three share the significand M, so each element's quotient u = |y| * (1/M) is formed once
+// and fed to the three conversions (scales 2^E, 2^(E+1), 2^(E+2)).  Element-major order keeps
+// two quotients live instead of sixteen.  Each loss is the same binary32 operation sequence
+// as cand_loss (even and odd elements in two chains, added at the end), so the values are
+// bit-identical; a code past 126 has NaN in M and cvs and scores NaN as there.
+template <bool WEIGHTED, int LPB, int NC>
+__device__ __forceinline__ void significand_group_losses(const float (&y)[kLaneElems],
+                                                         const float (&w)[kLaneElems],
+                                                         const Scale* tab, int cb, int d,
+                                                         float (&J)[NC]) {
+    constexpr int KMAX = (NC + 7) / 8;
+    const float rM = tab[cb + d].rM;
+    float M[KMAX], cvs[KMAX], acc0[KMAX], acc1[KMAX];
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+        if (d + 8 * k < NC) {
+            M[k] = tab[cb + d + 8 * k].M;
+            cvs[k] = tab[cb + d + 8 * k].cvs;
+        }
+        acc0[k] = 0.f;
+        acc1[k] = 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < kLaneElems; i += 2) {
+        float u0 = fabsf(y[i]) * rM, u1 = fabsf(y[i + 1]) * rM;
+        // not rematerializable: the compiler would otherwise recompute them per candidate
+        asm volatile("" : "+v"(u0), "+v"(u1));
+#pragma unroll
+        for (int k = 0; k < KMAX; ++k) {
+            if (d + 8 * k >= NC) continue;
+            const uint32_t p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(any_bits(), u0, u1, cvs[k], 0);
+            const float2v g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(p, cvs[k], 0);
+            const float e0 = fmaf(-g.x, M[k], fabsf(y[i]));
+            const float e1 = fmaf(-g.y, M[k], fabsf(y[i + 1]));
+            if (WEIGHTED) {
+                acc0[k] = fmaf(w[i] * e0, e0, acc0[k]);
+                acc1[k] = fmaf(w[i + 1] * e1, e1, acc1[k]);
+            } else {
+                acc0[k] = fmaf(e0, e0, acc0[k]);
+                acc1[k] = fmaf(e1, e1, acc1[k]);
+            }
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k)
+        if (d + 8 * k < NC) J[d + 8 * k] = group_sum<LPB>(acc0[k] + acc1[k]);
+}
+
+// max(|a|, |b|, c) in one instruction (abs source modifiers); c >= 0.  The inputs come from
+// arithmetic, so none is a signaling NaN and no canonicalization is needed.
+__device__ __forceinline__ float max3_abs(float a, float b, float c) {
+    float r;
+    asm("v_max3_f32 %0, |%1|, |%2|, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
+
 // Exactly rounded u = RN32(v / M) for M in [1, 2) with rM = RN32(1 / M) (Markstein): the
 // remainder u M - v is exact in one fused multiply-add and corrects u once.  Written as
 // u - (u M - v) rM so that a zero quotient keeps the sign of v (-0 + -0 = -0), which the
@@ -415,11 +472,10 @@ struct Params {
     float denom;              // 6 D, for kScaleSlots
     const uint32_t* ws;       // workspace of the dynamic path
     float* tensor_scale;      // static and slot paths: written once, by the first lane of the grid
-    const uint4* nx;          // batched calls: the next tensor, whose |x| maximum the first
-    int64_t nx_vec;           //   nx_wgs workgroups of the grid reduce into nx_slots (nx_vec
-    int64_t nx_per;           //   16-byte vectors, nx_per per workgroup); nx_wgs = 0: none
+    const uint4* nx;          // batched calls: the next tensor, whose |x| maximum every
+    int64_t nx_vec;           //   workgroup reduces a share of (nx_per of its nx_vec 16-byte
+    int64_t nx_per;           //   vectors) into nx_slots; nx_per = 0: no next tensor
     uint32_t* nx_slots;
-    uint32_t nx_wgs;
     int win_tight;            // window variants: per-mantissa offsets (else win_lo..win_hi)
     int win_lo, win_hi;
     int swizzled;             // scales in 128 x 4 tiles (else row-major)
@@ -538,37 +594,40 @@ __device__ int choose_window(const float (&y)[kLaneElems], const float (&w)[kLan
     return dstar < ncand ? lo + dstar : lo;   // dstar >= ncand only if every loss is NaN
 }
 
-// Batched calls: a reducer workgroup of the quantization grid streams its share of the next
-// tensor (16 vectors of 16 bytes in flight per lane) and raises slot blockIdx mod 64 of that
-// tensor's workspace with one relaxed device-scope atomic maximum; the next kernel on the
-// stream folds the slots after this grid has completed.  The reducers are the first
-// workgroups of the grid, so they are dispatched first and stream while the other
-// workgroups of the grid run the arithmetic-bound sweep beside them.
+// Batched calls: every workgroup of a quantization grid also reads an equal share of the
+// next tensor (at most 4 loads of 16 bytes per lane in flight, issued behind the tile's own
+// loads) and each wave raises slot (4 * workgroup + wave) mod 64 of that tensor's workspace
+// with one relaxed device-scope atomic maximum; the next kernel on the stream folds the slots
+// after this grid has completed.  Spread this way the next tensor streams at a modest rate
+// for the whole sweep; dedicated reducer workgroups at the head of the grid instead burst
+// it at full bandwidth, queueing the first sweep tiles' loads and holding wave slots.
 template <typename In>
-__device__ void reduce_share(const Params& p) {
-    const int64_t b0 = (int64_t)blockIdx.x * p.nx_per;
-    const int64_t b1 = min(b0 + p.nx_per, p.nx_vec);
+__device__ __forceinline__ uint32_t next_share_max(const Params& p, uint32_t tile) {
+    const int64_t v0 = (int64_t)tile * p.nx_per;
+    const int64_t v1 = min(v0 + p.nx_per, p.nx_vec);
     uint32_t m = 0;
-    int64_t i = b0 + threadIdx.x;
-    for (; i + 15 * kThreads < b1; i += 16 * kThreads) {
-        uint4 d[16];
+    for (int64_t v = v0 + threadIdx.x; v < v1; v += 4 * kThreads) {
+        uint4 d[4];
 #pragma unroll
-        for (int k = 0; k < 16; ++k) d[k] = p.nx[i + k * kThreads];
+        for (int k = 0; k < 4; ++k)
+            d[k] = v + k * kThreads < v1 ? p.nx[v + k * kThreads] : make_uint4(0u, 0u, 0u, 0u);
 #pragma unroll
-        for (int k = 0; k < 16; ++k) m = max(m, absmax_bits(d[k], In()));
+        for (int k = 0; k < 4; ++k) m = max(m, absmax_bits(d[k], In()));
     }
-    for (; i < b1; i += kThreads) m = max(m, absmax_bits(p.nx[i], In()));
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off, 64));
-    __shared__ uint32_t s_red[kThreads / 64];
-    if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = m;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        m = max(max(s_red[0], s_red[1]), max(s_red[2], s_red[3]));
-        if (m != 0u)
-            __hip_atomic_fetch_max(p.nx_slots + (blockIdx.x & (kSlots - 1)) * kSlotStride, m,
-                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    return m;
+}
+
+__device__ __forceinline__ void raise_next_slot(const Params& p, uint32_t tile, uint32_t m) {
+    // wave maximum: xor exchanges inside 32-lane halves, then the two halves' lane 0
+    m = max(m, (uint32_t)__builtin_amdgcn_ds_swizzle((int)m, (1 << 10) | 0x1F));
+    m = max(m, (uint32_t)__builtin_amdgcn_ds_swizzle((int)m, (2 << 10) | 0x1F));
+    m = max(m, (uint32_t)__builtin_amdgcn_ds_swizzle((int)m, (4 << 10) | 0x1F));
+    m = max(m, (uint32_t)__builtin_amdgcn_ds_swizzle((int)m, (8 << 10) | 0x1F));
+    m = max(m, (uint32_t)__builtin_amdgcn_ds_swizzle((int)m, (16 << 10) | 0x1F));
+    m = max((uint32_t)__builtin_amdgcn_readlane((int)m, 0), (uint32_t)__builtin_amdgcn_readlane((int)m, 32));
+    if ((threadIdx.x & 63) == 0 && m != 0u)
+        __hip_atomic_fetch_max(p.nx_slots + ((tile * 4u + (threadIdx.x >> 6)) & (kSlots - 1)) * kSlotStride,
+                               m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <int METHOD, typename In, int N>
@@ -580,11 +639,7 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
     constexpr bool WEIGHTED_OBJ = METHOD == kSweepWmse || METHOD == kFourSix || METHOD == kWindowWmse;
     __shared__ Scale tab_all[kTabSize];
     Scale* tab = tab_all + kTabLo;                 // tab[c] for codes c in -16..143
-    if (blockIdx.x < p.nx_wgs) {        // uniform per workgroup
-        reduce_share<In>(p);
-        return;
-    }
-    const uint32_t tile = blockIdx.x - p.nx_wgs;      // the workgroup's tile of this tensor
+    const uint32_t tile = blockIdx.x;                 // the workgroup's tile of this tensor
     const int lane = threadIdx.x & 63;
     const int64_t gtid = (int64_t)tile * kThreads + threadIdx.x;
     const int64_t blk = gtid / LPB;
@@ -612,6 +667,7 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
         for (int i = 0; i < kLaneElems; ++i) w[i] = 1.0f;
     }
     fill_scale_table<METHOD == kAbsMax || METHOD == kFourSix>(tab_all);
+    if (p.nx_per > 0) raise_next_slot(p, tile, next_share_max<In>(p, tile));   // uniform
     __shared__ float s_scale[2];
     if (p.scale_src == kScaleSlots && threadIdx.x < 64) {
         // the slots were raised by the previous kernel on the stream: wave 0 folds them
@@ -654,7 +710,7 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
     }
     float ymax = 0.f;
 #pragma unroll
-    for (int i = 0; i < kLaneElems; i += 2) ymax = fmaxf(ymax, fmaxf(fabsf(y[i]), fabsf(y[i + 1])));
+    for (int i = 0; i < kLaneElems; i += 2) ymax = max3_abs(y[i], y[i + 1], ymax);
     ymax = group_max<LPB>(ymax);
 
     // ---- choose the block scale code ---------------------------------------------------
@@ -702,17 +758,8 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
         if (__all(cb >= 8)) {
             // normal codes only: c, c+8, c+16 share the significand M and differ in 2^E
 #pragma unroll
-            for (int d = 0; d < 8 && d < NC; ++d) {
-                const Scale s0 = tab[cb + d];
-                float u[kLaneElems];
-#pragma unroll
-                for (int i = 0; i < kLaneElems; ++i) u[i] = fabsf(y[i]) * s0.rM;
-#pragma unroll
-                for (int j = d; j < NC; j += 8) {
-                    const Scale sj = tab[cb + j];
-                    J[j] = group_sum<LPB>(cand_loss<WGT>(u, y, w, sj.cvs, sj.M));
-                }
-            }
+            for (int d = 0; d < 8 && d < NC; ++d)
+                significand_group_losses<WGT, LPB, NC>(y, w, tab, cb, d, J);
         } else {
 #pragma unroll
             for (int d = 0; d < NC; ++d) {
@@ -894,16 +941,9 @@ int64_t quant_grid(const Call& c) {
     return (lanes + kThreads - 1) / kThreads;
 }
 
-// Reducer workgroups for a next tensor of nvec 16-byte vectors: one per 64 KiB, at most one
-// per CU (each keeps 64 KiB in flight, so 256 of them saturate HBM).
-int64_t reducer_wgs(int64_t nvec) {
-    const int64_t r = (nvec + 4095) / 4096;
-    return r < 256 ? r : 256;
-}
-
 template <int METHOD, typename In, int N>
 hipError_t launch_quant(const Call& c, const Params& p) {
-    const int64_t grid = quant_grid(c) + p.nx_wgs;              // reducers, then one per tile
+    const int64_t grid = quant_grid(c);
     hipLaunchKernelGGL((quant_kernel<METHOD, In, N>), dim3((unsigned)grid), dim3(kThreads), 0, c.stream,
                        static_cast<const In*>(c.x), c.colw, c.q, c.scales, p);
     return hipGetLastError();
@@ -1004,8 +1044,8 @@ hipError_t launch_main(const Call& c, hipStream_t stream, const Chain& chain = C
     p.tensor_scale = c.tensor_scale;
     p.nx = static_cast<const uint4*>(chain.nx);
     p.nx_vec = chain.nx ? chain.nx_bytes / 16 : 0;
-    p.nx_wgs = (uint32_t)reducer_wgs(p.nx_vec);
-    p.nx_per = p.nx_wgs ? (p.nx_vec + p.nx_wgs - 1) / p.nx_wgs : 0;
+    const int64_t tiles = quant_grid(c);
+    p.nx_per = p.nx_vec > 0 ? (p.nx_vec + tiles - 1) / tiles : 0;
     p.nx_slots = chain.nx_ws ? chain.nx_ws + kSlotWord0 : nullptr;
     p.swizzled = c.layout == NVFP4_SCALES_SWIZZLED ? 1 : 0;
     p.sw_kt = (uint32_t)((c.cols / c.block + 3) / 4);
