@@ -325,6 +325,26 @@ def test_batched_zero_and_nonfinite_tensors(nv, method):
     _assert_batched_equals_single(nv, method, xs, ws, outs)
 
 
+@pytest.mark.parametrize("where", ["first", "middle", "last"])
+def test_batched_next_share_covers_every_vector(nv, where):
+    """Every workgroup of a quantization kernel reduces an equal share of the next tensor; a
+    single planted maximum at the first, a middle or the last element of a tensor much larger
+    than its predecessor (shares of many vectors per lane, a ragged last share) must reach
+    that tensor's S."""
+    xs, ws = _batch_inputs([(3, 48), (1000, 4128), (2, 64)], 12)
+    big = xs[1].clone()
+    flat = big.view(-1)
+    idx = {"first": 0, "middle": flat.numel() // 2 + 7, "last": flat.numel() - 1}[where]
+    flat[idx] = -37.5                                     # |x| maximum of the tensor
+    xs[1] = big
+    for method in ("absmax", "scalesweep_wmse"):
+        outs = nv.quantize_batched(xs, method, 16, weights=ws if method.endswith("wmse") else None)
+        torch.cuda.synchronize()
+        d = 448.0 if method == "absmax" else 256.0
+        assert outs[1][2].item() == np.float32(37.5) / np.float32(6.0 * d)
+        _assert_batched_equals_single(nv, method, xs, ws, outs)
+
+
 def test_batched_many_tensors(nv):
     """More tensors than the host's fixed chain array holds (the heap path)."""
     g = workloads.generator(DEV, 10, 10)
