@@ -119,6 +119,25 @@ def measure_rows(nv, workloads, torch, dev, layer):
     out["f1_reference_scales"] = {"workload": "q_proj [4096, 4096] bf16, WMSE weights", **ref,
                                   "gaps_wmse": {k: round(v, 5) for k, v in gaps.items()}}
 
+    # block-size sweep on one 8192 x 8192 weight: time per call (dynamic S) and the objective
+    # gap of every rule to the optimal real block scale, for both objectives
+    x2, w2 = workloads.square8192(dev)
+    n2 = x2.numel()
+    sweep = {}
+    for blk in (16, 32, 64, 128):
+        per = {}
+        for m in ("absmax", "four_over_six", "scalesweep_mse", "scalesweep_wmse"):
+            wt = w2 if m in ("scalesweep_wmse",) else None
+            ms = _timed(torch, lambda: nv.quantize(x2, m, blk, weight=wt), 10)
+            per[m] = {"ms": round(ms, 4), "input_GBps": round(2 * n2 / ms / 1e6, 1)}
+        gaps_mse = nv.gap_report(x2, blk, None)
+        gaps_wmse = nv.gap_report(x2, blk, w2)
+        sweep[f"n{blk}"] = {**per, "gap_to_optimum_mse": {k: round(v, 5) for k, v in gaps_mse.items()},
+                            "gap_to_optimum_wmse": {k: round(v, 5) for k, v in gaps_wmse.items()}}
+    out["c2_block_sizes"] = {"workload": "one [8192, 8192] bf16 weight, dynamic S, WMSE weights of "
+                                         "8192 columns", **sweep}
+    del x2, w2
+
     t = workloads.online_tensors(dev)
     onl = {}
     for name in ("act", "k", "v", "q"):
@@ -127,6 +146,9 @@ def measure_rows(nv, workloads, torch, dev, layer):
             ms = _timed(torch, lambda: nv.quantize_online(xo, m, 0.002, 16, layout="swizzled"), 10)
             onl[f"{name}_{m}"] = {"shape": list(t[name].shape), "ms": round(ms, 4),
                                   "input_GBps": round(2 * xo.numel() / ms / 1e6, 1)}
+            ms = _timed(torch, lambda: nv.quantize(xo, m, 16), 10)
+            onl[f"{name}_{m}_dynamic_S"] = {"ms": round(ms, 4),
+                                            "input_GBps": round(2 * xo.numel() / ms / 1e6, 1)}
     g = workloads.generator(dev, 77)
     imp = workloads.column_importance(8192, g, dev, tokens=256)[None].contiguous()
     table8 = {}
