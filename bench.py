@@ -303,6 +303,22 @@ def main():
         torch.cuda.synchronize()
         launch_ms.append(e0.elapsed_time(e1) / reps)
     avg_launch_s = sum(launch_ms) / len(launch_ms) / 1e3
+    # the same launches with L2 and MALL flushed before each (a 512 MiB fill between launches)
+    flush = torch.empty(128 * 1024 * 1024, dtype=torch.float32, device=dev)
+    cold_ms = []
+    for i, x in enumerate(xs):
+        per = []
+        for r in range(reps):
+            flush.fill_(float(r))
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            nv.quantize(x, DOMINANT, 16, weight=ws_col[i], out=outs[DOMINANT][i],
+                        static_scale=scales_dyn[i])
+            e1.record(stream)
+            torch.cuda.synchronize()
+            per.append(e0.elapsed_time(e1))
+        cold_ms.append(sorted(per)[len(per) // 2])
+    del flush
     evals_per_launch = n_elem / len(xs) * CANDIDATES_16[DOMINANT]
     ops_per_launch = evals_per_launch * OPS_PER_EVAL[DOMINANT]
     achieved = ops_per_launch / avg_launch_s / 1e12
@@ -312,6 +328,7 @@ def main():
         "unit": "TOP/s", "frac": round(achieved / VALU_PEAK_TOPS, 3),
         "traffic": read_traffic(),
         "kernel": DOMINANT_SYMBOL, "avg_launch_us": round(avg_launch_s * 1e6, 2),
+        "avg_launch_us_cold": round(sum(cold_ms) / len(cold_ms) * 1e3, 2),
         "algorithmic_ops_per_launch": int(ops_per_launch),
         "hbm_GBps_algorithmic": round(alg_bytes / avg_launch_s / 1e9, 1),
         "hbm_frac": round(alg_bytes / avg_launch_s / 1e9 / HBM_PEAK_GBS, 3),
