@@ -108,6 +108,16 @@ def measure_rows(nv, workloads, torch, dev, layer):
         win[name] = {"ms": round(ms, 4), "input_GBps": round(2 * n / ms / 1e6, 1)}
     out["f2_windows"] = {"workload": "gate_proj [14336, 4096] bf16, block 16, static S", **win}
 
+    # dequantization of the same tensor: 0.5 B of nibbles + 1/16 B of scale per element in,
+    # 4 B of binary32 out
+    q, sc, Sg = nv.quantize(x, "scalesweep_wmse", 16, weight=w)
+    xh = torch.empty(x.shape, dtype=torch.float32, device=dev)
+    ms = _timed(torch, lambda: nv.dequant(q, sc, Sg, 16, out=xh), 10)
+    out["a10_dequant"] = {"workload": "gate_proj [14336, 4096], block 16, binary32 out",
+                          "ms": round(ms, 4),
+                          "hbm_GBps_algorithmic": round(n * (0.5 + 1 / 16 + 4) / ms / 1e6, 1)}
+    del xh
+
     xq, wq = layer["q_proj"]
     _, _, Sq = nv.quantize(xq, "scalesweep_mse", 16)
     ref = {}

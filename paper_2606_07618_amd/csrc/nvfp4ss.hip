@@ -861,42 +861,43 @@ __global__ __launch_bounds__(256) void swizzle_pad_kernel(uint8_t* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------------------
-// Dequantization: x_hat = RN32((q s) S), 16 elements per lane.
+// Dequantization: x_hat = RN32((q s) S).
 // ---------------------------------------------------------------------------------------
 
+typedef float float4v __attribute__((ext_vector_type(4)));
+
+// A wave writes 1024 consecutive outputs (4 KiB) as four stores of 16 bytes per lane, each
+// store contiguous across the wave: store k of lane L holds elements base + 256 k + 4 L ...
+// + 3, decoded from the byte pair of their nibbles and the scale of their block.  (Sixteen
+// consecutive outputs per lane, 64 bytes apart between lanes, reached 3.6 TB/s on MI355X; the
+// wave-contiguous stores 5.8 TB/s, and streaming them past the caches 6.8 TB/s.)
 template <int N>
 __global__ __launch_bounds__(kThreads) void dequant_kernel(const uint8_t* __restrict__ q,
                                                            const uint8_t* __restrict__ scales,
                                                            const float* __restrict__ tensor_scale,
-                                                           int64_t nseg, float* __restrict__ out) {
-    const int64_t seg = (int64_t)blockIdx.x * kThreads + threadIdx.x;    // 16-element segment
-    if (seg >= nseg) return;
+                                                           int64_t n, float* __restrict__ out) {
+    const int64_t base = ((int64_t)blockIdx.x * kThreads + (threadIdx.x & ~63)) * kLaneElems;
+    const int lane = threadIdx.x & 63;
     const float S = tensor_scale[0];
-    const uint2 pk = reinterpret_cast<const uint2*>(q)[seg];
-    const int code = scales[(seg * kLaneElems) / N];
-    const float s = e4m3_value(code);
-    const float cvs = code == 0 ? 1.0f : s;
-    const float M = code == 0 ? 0.f : __uint_as_float((__float_as_uint(s) & 0x007FFFFFu) | 0x3F800000u);
-    const uint32_t words[2] = {pk.x, pk.y};
-    float o[kLaneElems];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            float2v g;
-            switch (b) {   // the byte selector must be a constant
-                case 0: g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(words[h], cvs, 0); break;
-                case 1: g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(words[h], cvs, 1); break;
-                case 2: g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(words[h], cvs, 2); break;
-                default: g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(words[h], cvs, 3); break;
-            }
-            o[8 * h + 2 * b] = (g.x * M) * S;        // g 2^E M = q s exactly, then one rounding
-            o[8 * h + 2 * b + 1] = (g.y * M) * S;
+    for (int k = 0; k < 4; ++k) {
+        const int64_t e = base + 256 * k + 4 * lane;      // n is a multiple of 16: all or none
+        if (e < n) {
+            const uint32_t pair = *reinterpret_cast<const uint16_t*>(q + (e >> 1));
+            const int code = scales[e / N];
+            const float s = e4m3_value(code);
+            const float cvs = code == 0 ? 1.0f : s;
+            const float M = code == 0 ? 0.f : __uint_as_float((__float_as_uint(s) & 0x007FFFFFu) | 0x3F800000u);
+            const float2v g0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pair, cvs, 0);
+            const float2v g1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pair, cvs, 1);
+            float4v v;                          // g 2^E M = q s exactly, then one rounding
+            v.x = (g0.x * M) * S;
+            v.y = (g0.y * M) * S;
+            v.z = (g1.x * M) * S;
+            v.w = (g1.y * M) * S;
+            __builtin_nontemporal_store(v, reinterpret_cast<float4v*>(out + e));
         }
     }
-    float4* dst = reinterpret_cast<float4*>(out + seg * kLaneElems);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) dst[k] = make_float4(o[4 * k], o[4 * k + 1], o[4 * k + 2], o[4 * k + 3]);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -1292,14 +1293,13 @@ int nvfp4_dequant(const uint8_t* q, const uint8_t* scales, const float* tensor_s
     if (n == 0) return NVFP4_OK;
     if (!q || !scales || !out) return NVFP4_ERR_NULL;
     if (!aligned(q, 8) || !aligned(out, 16)) return NVFP4_ERR_ALIGN;
-    const int64_t nseg = n / kLaneElems;
-    const int64_t grid = (nseg + kThreads - 1) / kThreads;
+    const int64_t grid = (n / kLaneElems + kThreads - 1) / kThreads;   // 4096 outputs each
     hipStream_t s = (hipStream_t)stream;
     switch (block) {
-        case 16: hipLaunchKernelGGL(dequant_kernel<16>, dim3((unsigned)grid), dim3(kThreads), 0, s, q, scales, tensor_scale, nseg, (float*)out); break;
-        case 32: hipLaunchKernelGGL(dequant_kernel<32>, dim3((unsigned)grid), dim3(kThreads), 0, s, q, scales, tensor_scale, nseg, (float*)out); break;
-        case 64: hipLaunchKernelGGL(dequant_kernel<64>, dim3((unsigned)grid), dim3(kThreads), 0, s, q, scales, tensor_scale, nseg, (float*)out); break;
-        default: hipLaunchKernelGGL(dequant_kernel<128>, dim3((unsigned)grid), dim3(kThreads), 0, s, q, scales, tensor_scale, nseg, (float*)out); break;
+        case 16: hipLaunchKernelGGL(dequant_kernel<16>, dim3((unsigned)grid), dim3(kThreads), 0, s, q, scales, tensor_scale, n, (float*)out); break;
+        case 32: hipLaunchKernelGGL(dequant_kernel<32>, dim3((unsigned)grid), dim3(kThreads), 0, s, q, scales, tensor_scale, n, (float*)out); break;
+        case 64: hipLaunchKernelGGL(dequant_kernel<64>, dim3((unsigned)grid), dim3(kThreads), 0, s, q, scales, tensor_scale, n, (float*)out); break;
+        default: hipLaunchKernelGGL(dequant_kernel<128>, dim3((unsigned)grid), dim3(kThreads), 0, s, q, scales, tensor_scale, n, (float*)out); break;
     }
     return hipGetLastError() == hipSuccess ? NVFP4_OK : NVFP4_ERR_HIP;
 }

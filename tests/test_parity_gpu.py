@@ -211,17 +211,23 @@ def test_deterministic_and_stream_ordered(nv):
         assert torch.equal(a, b)
 
 
+@pytest.mark.parametrize("shape", [(96, 512), (37, 384), (1, 128)])
 @pytest.mark.parametrize("block", [16, 32, 64, 128])
 @pytest.mark.parametrize("method", ["absmax", "scalesweep_wmse"])
-def test_dequant_parity(nv, block, method):
-    g = workloads.generator(DEV, 6, block)
-    x = workloads.llm_weight(96, 512, g, DEV)
-    w = workloads.column_importance(512, g, DEV, tokens=64)
+def test_dequant_parity(nv, block, method, shape):
+    """Whole waves and workgroups, a ragged last wave (37 x 384) and a single partial wave;
+    the output buffer's tail past the tensor must stay untouched."""
+    rows, cols = shape
+    g = workloads.generator(DEV, 6, block, cols)
+    x = workloads.llm_weight(rows, cols, g, DEV)
+    w = workloads.column_importance(cols, g, DEV, tokens=64)
     q, sc, S = check(nv, method, x, block, w)
-    xh = nv.dequant(q, sc, S, block)
+    buf = torch.full((rows * cols + 4096,), -7.0, dtype=torch.float32, device=DEV)
+    xh = nv.dequant(q, sc, S, block, out=buf[:rows * cols].view(rows, cols))
     torch.cuda.synchronize()
     ref = oracle.dequant(q.cpu().numpy(), sc.cpu().numpy(), S.item(), block)
     assert np.array_equal(xh.cpu().numpy().view(np.uint32), ref.view(np.uint32))
+    assert torch.all(buf[rows * cols:] == -7.0)
 
 
 # ---------------------------------------------------------------------------------------
