@@ -31,7 +31,8 @@ sys.path.insert(0, str(ROOT))
 
 # MI355X figures used for the rooflines.
 HBM_PEAK_GBS = 8000.0
-VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12        # 39.32 T lane-ops/s (no packed FP32)
+# binary32 vector: 157.3 TFLOP/s published = 256 CU x 4 SIMD x 32 lanes x 2.4 GHz lane-ops
+VALU_PEAK_TOPS = 256 * 4 * 32 * 2.4e9 / 1e12    # 78.64 T lane-ops/s (an FMA is one lane-op)
 # Algorithmic VALU lane-operations per element-candidate evaluation: scale, round,
 # reconstruct-and-subtract, square-and-accumulate (+ one weight multiply for WMSE).
 OPS_PER_EVAL = {"scalesweep_mse": 4, "scalesweep_wmse": 5}
