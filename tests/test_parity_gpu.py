@@ -288,10 +288,10 @@ def _batch_inputs(shapes, seed):
     return xs, ws
 
 
-def _assert_batched_equals_single(nv, method, xs, ws, outs):
+def _assert_batched_equals_single(nv, method, xs, ws, outs, block=16):
     use_w = method in ("scalesweep_wmse", "four_over_six")
     for k, x in enumerate(xs):
-        q1, sc1, S1 = nv.quantize(x, method, 16, weight=ws[k] if use_w else None)
+        q1, sc1, S1 = nv.quantize(x, method, block, weight=ws[k] if use_w else None)
         torch.cuda.synchronize()
         q2, sc2, S2 = outs[k]
         assert torch.equal(S1, S2) or (torch.isnan(S1).all() and torch.isnan(S2).all()), k
@@ -329,6 +329,27 @@ def test_batched_zero_and_nonfinite_tensors(nv, method):
     assert outs[1][2].item() == 1.0
     assert np.isnan(outs[2][2].item())
     _assert_batched_equals_single(nv, method, xs, ws, outs)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("block", [32, 128])
+@pytest.mark.parametrize("method", METHODS)
+def test_batched_other_blocks_and_f32(nv, method, block, dtype):
+    """The chain with multi-lane blocks and binary32 input (4-byte elements: a next tensor's
+    share is twice as many 16-byte vectors per element)."""
+    xs, ws = _batch_inputs([(96, 384), (7, 1152), (300, 256), (0, 128)], 13)
+    if dtype == "f32":
+        xs = [x.float() for x in xs]
+    use_w = method in ("scalesweep_wmse", "four_over_six")
+    outs = nv.quantize_batched(xs, method, block, weights=ws if use_w else None)
+    _assert_batched_equals_single(nv, method, xs, ws, outs, block)
+    big = 2
+    check_w = ws[big].cpu().numpy() if use_w else None
+    S_ref, q_ref, sc_ref = oracle.quantize(method, workloads.host_array(xs[big]), block,
+                                           RANGE[method], 0.0, check_w)
+    assert outs[big][2].item() == S_ref
+    assert np.array_equal(outs[big][1].cpu().numpy(), sc_ref)
+    assert np.array_equal(outs[big][0].cpu().numpy(), q_ref)
 
 
 @pytest.mark.parametrize("where", ["first", "middle", "last"])
