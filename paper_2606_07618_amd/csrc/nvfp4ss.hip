@@ -457,6 +457,26 @@ __device__ double exact_loss(const float (&y)[kLaneElems], const float (&w)[kLan
     return acc;
 }
 
+// Whether the scales s0 = M 2^E and s1 = M 2^(E+1) (codes c and c + 8) reconstruct every
+// element of the block identically: the exact E2M1 rounding of u = RN32(|y| / M) (the quotient
+// the emit uses) at both scales gives the same g 2^E for all n elements.  Then every term of the
+// loss, weighted or not, is the same for both codes, and so are the two sums.
+template <int LPB>
+__device__ bool same_reconstruction(const float (&y)[kLaneElems], const Scale& s0, const Scale& s1) {
+    uint32_t differ = 0u;
+#pragma unroll
+    for (int i = 0; i < kLaneElems; i += 2) {
+        const float u0 = div_by_significand(fabsf(y[i]), s0.M, s0.rM);
+        const float u1 = div_by_significand(fabsf(y[i + 1]), s0.M, s0.rM);
+        const float2v g0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(
+            __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, u0, u1, s0.cvs, 0), s0.cvs, 0);
+        const float2v g1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(
+            __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, u0, u1, s1.cvs, 0), s1.cvs, 0);
+        differ |= (__float_as_uint(g0.x) ^ __float_as_uint(g1.x)) | (__float_as_uint(g0.y) ^ __float_as_uint(g1.y));
+    }
+    return group_sum<LPB>(differ != 0u ? 1.0f : 0.0f) == 0.0f;
+}
+
 // ---------------------------------------------------------------------------------------
 // Global scale: max |x| over the tensor.
 // ---------------------------------------------------------------------------------------
@@ -879,20 +899,33 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
         const bool near = (seen2 >> lane) & 1ull;
         if (seen2 != 0ull) {
             if (near) {
-                double jb = 0.0;
-                int db = -1;
+                // candidates in the band; two of them eight codes apart (one significand,
+                // scales s and 2s) that reconstruct every element identically have equal
+                // exact losses, so the smaller code wins without summing in binary64
+                uint32_t inband = 0u;
+#pragma unroll
+                for (int d = 0; d < NC; ++d)
+                    if (J[d] <= bound && cb + d >= 1 && cb + d <= 126) inband |= 1u << d;
+                const int d0 = __builtin_ctz(inband | 0x80000000u), d1 = 31 - __builtin_clz(inband | 1u);
+                const bool pair8 = __builtin_popcount(inband) == 2 && d1 == d0 + 8;
+                if (pair8 && same_reconstruction<LPB>(y, tab[cb + d0], tab[cb + d1])) {
+                    dstar = d0;
+                } else {
+                    double jb = 0.0;
+                    int db = -1;
 #pragma unroll 1
-                for (int d = 0; d < NC; ++d) {
-                    if (J[d] <= bound && cb + d >= 1 && cb + d <= 126) {
-                        const Scale sd = tab[clamp_code(cb + d)];
-                        const double jd = exact_loss<WGT, LPB>(y, w, sd, part, group_base);
-                        if (db < 0 || jd < jb) {
-                            jb = jd;
-                            db = d;
+                    for (int d = 0; d < NC; ++d) {
+                        if ((inband >> d) & 1u) {
+                            const Scale sd = tab[cb + d];
+                            const double jd = exact_loss<WGT, LPB>(y, w, sd, part, group_base);
+                            if (db < 0 || jd < jb) {
+                                jb = jd;
+                                db = d;
+                            }
                         }
                     }
+                    if (db >= 0) dstar = db;
                 }
-                if (db >= 0) dstar = db;
             }
         }
         code = clamp_code(cb + dstar);   // always a window code unless every loss is NaN
