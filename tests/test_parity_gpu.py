@@ -134,6 +134,55 @@ def test_parity_edges(nv, name, method, dtype):
         check(nv, method, x, 16, w, static=1.0)
 
 
+def _tie_blocks(n, count, seed):
+    """Blocks built around a normal E4M3 code c with scale s: n - 1 elements at 0, 2s, 3s or
+    4s and the largest at t s with t in [6.8, 7).  Codes c and c + 8 reconstruct every element
+    identically (2s, 3s, 4s and 6s at both scales), so their losses tie exactly and beat the
+    codes in between, and both lie in either window.  Every third block replaces one element
+    by 0.25 (1 + 2^-18) s, which code c rounds to s / 2 and code c + 8 to 0: c is better by a
+    relative margin far inside the re-scoring band.  Every third moves the largest element to
+    7 (1 + 2^-20) s, where c + 8 (8s) is better than c (6s) by such a margin.  binary32, S = 1."""
+    rng = np.random.default_rng(seed)
+    out = np.zeros((count, n), dtype=np.float32)
+    for b in range(count):
+        c = int(rng.integers(16, 118))
+        s = oracle.e4m3(c)
+        t = rng.choice([0.0, 2.0, 3.0, 4.0], size=n)
+        top = int(rng.integers(n))
+        t[top] = rng.uniform(6.8, 7.0) if b % 3 != 2 else 7.0 * (1 + 2.0 ** -20)
+        if b % 3 == 1:
+            t[(top + 1) % n] = 0.25 * (1 + 2.0 ** -18)
+        out[b] = (t * s * np.where(rng.random(n) < 0.5, -1.0, 1.0)).astype(np.float32)
+    return out
+
+
+@pytest.mark.parametrize("method", ["scalesweep_mse", "scalesweep_wmse"])
+@pytest.mark.parametrize("block", [16, 32])
+def test_parity_exact_and_near_ties(nv, method, block):
+    """Codes c and c + 8 tied exactly, or within far less than the re-scoring band: the
+    kernel must pick the oracle's code in every block (the smaller one on a tie)."""
+    blocks = _tie_blocks(block, 3 * 512, seed=block)
+    x = blocks.reshape(-1, 256)
+    w = np.random.default_rng(5).uniform(0.2, 3.0, 256).astype(np.float32)
+    # the construction does what it says: many blocks have c, c + 8 as their two best codes
+    # with equal losses, and many with losses within 2^-14 but unequal
+    L = oracle.window_lower(method, block)
+    wblocks = np.tile(w, blocks.size // 256).reshape(blocks.shape)
+    ties = near = 0
+    for b in range(0, blocks.shape[0], 7):
+        wb = wblocks[b] if method.endswith("wmse") else None
+        r = oracle.block_sweep(np.abs(blocks[b]), wb, L, 7)
+        J = r["J"][r["lo"]:r["hi"] + 1]
+        order = np.argsort(J, kind="stable")
+        j1, j2 = J[order[0]], J[order[1]]
+        if abs(int(order[1]) - int(order[0])) == 8:
+            ties += j1 == j2
+            near += (j1 != j2) and (j2 - j1 <= 2.0 ** -14 * j1)
+    assert ties >= 30 and near >= 30, (ties, near)
+    xt = torch.from_numpy(x).to(DEV)
+    check(nv, method, xt, block, torch.from_numpy(w).to(DEV), static=1.0)
+
+
 @pytest.mark.parametrize("method", METHODS)
 def test_parity_saturating_static_scale(nv, method):
     """A static S far too small: block maxima beyond 6 * 448 saturate the scale code at 126
