@@ -408,6 +408,117 @@ __device__ __forceinline__ void significand_group_losses_sched(const float (&y)[
     }
 }
 
+// ---------------------------------------------------------------------------------------
+// Weighted ScaleSweep at n = 16 with provably losing candidates skipped.
+// ---------------------------------------------------------------------------------------
+
+// The remaining (block, candidate) items of a wave, compacted candidate-major: owner lane in
+// bits 5:0, candidate code in bits 12:6; each slot then receives its item's loss.
+constexpr int kPrunedLow = 7;                          // candidates d < 7 (offsets -8..-2)
+struct PrunedLds {
+    uint32_t item[kThreads / 64][64 * (kPrunedLow + 1)];   // one spare round for idle lanes
+};
+
+__device__ __forceinline__ float bperm(int src_lane, float v) {
+    return __int_as_float(__builtin_amdgcn_ds_bpermute(src_lane << 2, __float_as_int(v)));
+}
+
+__device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Losses J[d] of the WMSE window (codes cb + d, d = 0..15, offsets -8..7; all codes normal).
+//
+// Offsets -1..7 (d = 7..15; d = 7 and 15 share the significand) are scored in place for every
+// block.  Each lower candidate d < 7 has a scale s below s0 <= max|y| / 6, so the block's
+// largest element saturates to 6 s there and its term alone, w1 (y1 - 6 s)^2, bounds the
+// candidate's loss from below.  That term is computed in the operation order the sweep uses
+// for it (e = RN(y1 - 6 s), which the sweep's fused multiply-add also yields; then
+// RN(RN(w1 e) e)), and a binary32 sum of non-negative terms accumulated with fused
+// multiply-adds is never below any one of its products, so the sweep's loss of d is >= the
+// bound.  A candidate whose bound exceeds the best in-place loss by more than the re-scoring
+// band is therefore neither the binary32 minimum nor inside the band, and skipping it leaves
+// the argmin and the band decisions exactly as with the full sweep; it scores +inf.
+//
+// The remaining lower candidates of the wave (about 0.7 per block on Student-t weights) are
+// compacted candidate-major into one list and scored by all 64 lanes together, each lane
+// pulling its item's |y| and weights from the owner lane with ds_bpermute and leaving the loss
+// in the item's slot; a lane-local loop would cost the wave the largest count of its 64
+// blocks.  The losses are the operation sequence of cand_loss, bit-identical to in-place
+// scoring.  Called in uniform control flow with all 64 lanes of the wave running.
+template <int NC>
+__device__ __forceinline__ void pruned_wmse_losses(const float (&y)[kLaneElems], const float (&w)[kLaneElems],
+                                                   float ymax, bool active, const Scale* tab, int cb,
+                                                   float (&J)[NC], PrunedLds& lds) {
+    static_assert(NC == 16 && kPrunedLow == 7, "window offsets -8..7");
+#pragma unroll
+    for (int d = kPrunedLow; d < kPrunedLow + 8; ++d) {
+        significand_group_losses<true, 1, NC>(y, w, tab, cb, d, J);
+        // finished here, before the next group's quotients are formed: one group live at a time
+        asm volatile("" : "+v"(J[d]));
+        if (d + 8 < NC) asm volatile("" : "+v"(J[d + 8]));
+    }
+    asm volatile("" : "+v"(ymax));                  // the bounds below are formed after the sweep
+    float jb = J[kPrunedLow];
+#pragma unroll
+    for (int d = kPrunedLow + 1; d < NC; ++d) jb = fminf(jb, J[d]);   // NaN codes past 126 drop out
+    // inactive lanes (past the last block) keep nothing
+    const float thr = active ? fmaf(jb, kBand, jb) + kBandAbs : -__builtin_inff();
+    float w1 = 0.f;                                  // weight of an element with |y| = ymax
+#pragma unroll
+    for (int i = 0; i < kLaneElems; ++i) w1 = fabsf(y[i]) == ymax ? w[i] : w1;
+
+    const int lane = threadIdx.x & 63;
+    uint32_t* items = lds.item[threadIdx.x >> 6];
+    uint64_t bal[kPrunedLow];                        // wave-uniform: which lanes keep candidate d
+    uint32_t base[kPrunedLow], total = 0u;
+#pragma unroll
+    for (int d = 0; d < kPrunedLow; ++d) {
+        const float sd = e4m3_value(cb + d);
+        const float e = ymax - 6.0f * sd;            // 6 sd is exact
+        const float t = w1 * e;
+        const float lb = t * e;
+        const bool keep = !(lb > thr);
+        bal[d] = __ballot(keep);
+        base[d] = total;
+        if (keep) items[total + lanes_below(bal[d])] = (uint32_t)lane | ((uint32_t)(cb + d) << 6);
+        total += (uint32_t)__popcll(bal[d]);
+    }
+    if (total != 0u) {                               // uniform
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll 1
+        for (uint32_t r = 0; r < total; r += 64) {   // uniform; all lanes take part in the exchanges
+            const uint32_t pidx = r + (uint32_t)lane;
+            const uint32_t it = pidx < total ? items[pidx] : 0u;
+            const int owner = (int)(it & 63u);
+            const Scale sc = tab[(int)(it >> 6)];    // code 0 (no item): NaN entries, loss unused
+            float acc0 = 0.f, acc1 = 0.f;
+#pragma unroll
+            for (int i = 0; i < kLaneElems; i += 2) {
+                const float a0 = bperm(owner, fabsf(y[i])), a1 = bperm(owner, fabsf(y[i + 1]));
+                const float w0 = bperm(owner, w[i]), w1i = bperm(owner, w[i + 1]);
+                const float u0 = a0 * sc.rM, u1 = a1 * sc.rM;
+                const uint32_t pk = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(any_bits(), u0, u1, sc.cvs, 0);
+                const float2v g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pk, sc.cvs, 0);
+                const float e0 = fmaf(-g.x, sc.M, a0);
+                const float e1 = fmaf(-g.y, sc.M, a1);
+                acc0 = fmaf(w0 * e0, e0, acc0);
+                acc1 = fmaf(w1i * e1, e1, acc1);
+                if (i % 4 == 2) __builtin_amdgcn_sched_barrier(0);   // 8 exchanges in flight at most
+            }
+            items[pidx] = __float_as_uint(acc0 + acc1);   // slots past total: idle lanes, unread
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+#pragma unroll
+    for (int d = 0; d < kPrunedLow; ++d)
+        J[d] = (bal[d] >> lane) & 1u ? __uint_as_float(items[base[d] + lanes_below(bal[d])]) : __builtin_inff();
+}
+
 // max(|a|, |b|, c) in one instruction (abs source modifiers); c >= 0.  The inputs come from
 // arithmetic, so none is a signaling NaN and no canonicalization is needed.
 __device__ __forceinline__ float max3_abs(float a, float b, float c) {
@@ -857,7 +968,21 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
         const int c0 = floor_code(ymax, 6.0f, 1.0f / 6.0f, tab);
         const int cb = c0 - Win::L;                 // candidate d is code cb + d
         float J[NC];
-        if (__all(cb >= 8)) {
+        if constexpr (WGT && N == 16) {
+            __shared__ PrunedLds pl;
+            if (__all(cb >= 8)) {
+                pruned_wmse_losses<NC>(y, w, ymax, active, tab, cb, J, pl);
+            } else {
+#pragma unroll
+                for (int d = 0; d < NC; ++d) {
+                    const Scale sd = tab[cb + d];
+                    float u[kLaneElems];
+#pragma unroll
+                    for (int i = 0; i < kLaneElems; ++i) u[i] = fabsf(y[i]) * sd.rM;
+                    J[d] = group_sum<LPB>(cand_loss<WGT>(u, y, w, sd.cvs, sd.M));
+                }
+            }
+        } else if (__all(cb >= 8)) {
             // normal codes only: c, c+8, c+16 share the significand M and differ in 2^E
 #pragma unroll
             for (int d = 0; d < 8 && d < NC; ++d)
