@@ -982,6 +982,27 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
                     J[d] = group_sum<LPB>(cand_loss<WGT>(u, y, w, sd.cvs, sd.M));
                 }
             }
+        } else if (!WGT && N == 16 && __all(cb >= 8)) {
+            // MSE, offsets -3..7: the lowest candidate (d = 0, scored with offset 5 in one
+            // significand group) comes last and is skipped by the wave when no block needs it.
+            // Its scale is below max|y| / 6, so the largest element saturates there and
+            // RN(RN(y1 - 6 s)^2) bounds its loss from below (the bound of pruned_wmse_losses
+            // with w = 1): above the best other loss plus the band, the candidate can neither
+            // be the minimum nor enter the band, and it scores +inf.
+#pragma unroll
+            for (int d = 1; d < 8; ++d) significand_group_losses_sched<LPB, NC>(y, tab, cb, d, J);
+            float jb = J[1];
+#pragma unroll
+            for (int d = 2; d < NC; ++d)
+                if (d != 8) jb = fminf(jb, J[d]);
+            const float thr = active ? fmaf(jb, kBand, jb) + kBandAbs : -__builtin_inff();
+            const float e = ymax - 6.0f * e4m3_value(cb);   // 6 s is exact
+            if (__any(!(e * e > thr))) {
+                significand_group_losses_sched<LPB, NC>(y, tab, cb, 0, J);
+            } else {
+                J[0] = __builtin_inff();
+                significand_group_losses_sched<LPB, NC>(y, tab, cb, 8, J);   // offset 5 alone
+            }
         } else if (__all(cb >= 8)) {
             // normal codes only: c, c+8, c+16 share the significand M and differ in 2^E
 #pragma unroll
