@@ -183,6 +183,69 @@ def test_parity_exact_and_near_ties(nv, method, block):
     check(nv, method, xt, block, torch.from_numpy(w).to(DEV), static=1.0)
 
 
+def _lower_bound_tensor(rows, seed):
+    """[rows, 1024] binary32 for S = 1, one 64-block row per wave of the n = 16 kernels; block
+    magnitudes spread over 2^-3..2^3.  Row r % 4 == 0: each block's largest magnitude (1.3x the
+    rest) sits in its first column, whose WMSE weight is 0, so the saturation bound of every
+    lower candidate is 0 and all seven are scored for every block (7 items per block, seven
+    compaction rounds per wave).  1: flat-topped blocks, magnitudes uniform in [0.5, 1] (MSE
+    keeps offset -3 for about half of them).  2: Student-t (df 4).  3: uniform magnitudes with
+    the largest (1.3x) in the second column."""
+    rng = np.random.default_rng(seed)
+    x = np.zeros((rows, 1024), np.float64)
+    b = np.arange(64) * 16
+    for r in range(rows):
+        scale = 2.0 ** rng.uniform(-3, 3, 64).repeat(16)
+        kind = r % 4
+        if kind == 2:
+            v = rng.standard_t(4, 1024) * scale
+        else:
+            v = rng.uniform(0.5 if kind == 1 else 0.0, 1.0, 1024) * scale
+            if kind != 1:
+                v[b + (0 if kind == 0 else 1)] = 1.3 * scale[b]
+        x[r] = v * np.where(rng.random(1024) < 0.5, -1.0, 1.0)
+    w = rng.uniform(0.2, 3.0, 1024)
+    w[::16] = 0.0
+    return x.astype(np.float32), w.astype(np.float32)
+
+
+@pytest.mark.parametrize("method", ["scalesweep_mse", "scalesweep_wmse"])
+def test_parity_lower_candidate_bound(nv, method):
+    """The n = 16 sweeps skip a lower window candidate when the saturated term of the block's
+    largest element already exceeds the best other loss by the re-scoring band.  WMSE: rows
+    where every block keeps all seven lower candidates (several compaction rounds per wave)
+    and rows where some do; MSE: waves that score offset -3 and waves that skip it; a ragged
+    last workgroup."""
+    x, w = _lower_bound_tensor(37, seed=11)
+    # the construction does what it says (oracle losses; the bound of a lower code c is
+    # w1 (y1 - 6 s_c)^2, compared with the best loss of the codes the kernel scores first)
+    wmse = method.endswith("wmse")
+    L = oracle.window_lower(method, 16)
+    kept_rows = {k: [] for k in range(4)}
+    for r in range(x.shape[0]):
+        kept = 0
+        for blk in range(64):
+            y = np.abs(x[r, 16 * blk:16 * blk + 16]).astype(np.float64)
+            wb = w[16 * blk:16 * blk + 16].astype(np.float64) if wmse else np.ones(16)
+            res = oracle.block_sweep(y, wb if wmse else None, L, 7)
+            c0 = res["c0"]
+            first = c0 - 1 if wmse else c0 - 2          # codes scored before the bound
+            jb = min(res["J"][c] for c in range(first, res["hi"] + 1) if wmse or c != c0 + 5)
+            i1 = int(np.argmax(y))
+            for c in range(res["lo"], first):
+                e = y[i1] - 6.0 * oracle.e4m3(c)
+                kept += wb[i1] * e * e <= jb * (1 + 2.0 ** -14)
+        kept_rows[r % 4].append(int(kept))
+    if wmse:
+        assert all(k == 64 * 7 for k in kept_rows[0]), kept_rows[0]
+        others = kept_rows[1] + kept_rows[2] + kept_rows[3]
+        assert max(others) < 64 * 7 and sum(k > 64 for k in others) >= 3, kept_rows
+    else:
+        per_row = [k for ks in kept_rows.values() for k in ks]
+        assert sum(k > 0 for k in per_row) >= 5 and sum(k == 0 for k in per_row) >= 5, kept_rows
+    check(nv, method, torch.from_numpy(x).to(DEV), 16, torch.from_numpy(w).to(DEV), static=1.0)
+
+
 @pytest.mark.parametrize("method", METHODS)
 def test_parity_saturating_static_scale(nv, method):
     """A static S far too small: block maxima beyond 6 * 448 saturate the scale code at 126
