@@ -53,6 +53,11 @@ def parse():
                     help="also run a plain device copy of known size (for counter scaling)")
     ap.add_argument("--no-rows", action="store_true",
                     help="skip the window / reference-scale / online / GPTQ measurements")
+    ap.add_argument("--profile-config", choices=("c0", "c2", "c3", "c4"), default=None,
+                    help="run only one other configuration's launches (a few of each, for "
+                         "rocprofv3 counter runs) and exit: c0 the FP32 1024x1024 matrix, c2 the "
+                         "8192x8192 block-size sweep, c3 the online tensors, c4 one "
+                         "Llama-3-70B-shaped layer")
     ap.add_argument("--c4-layers", type=int, default=2,
                     help="Llama-3-70B-shaped layers to stream through the WMSE quantizer "
                          "(80 is the whole model)")
@@ -225,6 +230,53 @@ def measure_llama70b(nv, workloads, torch, dev, layers):
             "extrapolated_80_layers_s": round(total_ms / layers * 80 / 1e3, 2)}
 
 
+def profile_config(name, nv, workloads, torch, dev, copy_calibration):
+    """The launches of one configuration, three of each, for counter runs (rocprofv3 groups
+    its dispatches by kernel and grid).  Inputs as in the timed measurements."""
+    reps = 3
+    ran = []
+
+    def run(label, fn):
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        ran.append(label)
+
+    if name == "c0":
+        x = torch.from_numpy(workloads.c0_matrix()).to(dev)
+        run("c0 fp32 [1024, 1024] scalesweep_mse D=448 dynamic",
+            lambda: nv.quantize(x, "scalesweep_mse", 16, fp8_range=448.0))
+    elif name == "c2":
+        x, w = workloads.square8192(dev)
+        for blk in (16, 32, 64, 128):
+            for m in ("absmax", "four_over_six", "scalesweep_mse", "scalesweep_wmse"):
+                wt = w if m == "scalesweep_wmse" else None
+                run(f"c2 [8192, 8192] n={blk} {m} dynamic",
+                    lambda: nv.quantize(x, m, blk, weight=wt))
+    elif name == "c3":
+        t = workloads.online_tensors(dev)
+        for nm in ("act", "k", "v", "q"):
+            xo = t[nm].reshape(-1, t[nm].shape[-1])
+            for m in ("absmax", "scalesweep_mse"):
+                run(f"c3 {nm} {list(t[nm].shape)} {m} static S swizzled",
+                    lambda: nv.quantize_online(xo, m, 0.002, 16, layout="swizzled"))
+    else:
+        lay = workloads.llama70b_layer(0, dev)
+        xs = [lay[n][0] for n in lay]
+        ws_ = [lay[n][1] for n in lay]
+        outs = [nv.quantize(x, "scalesweep_wmse", 16, weight=w) for x, w in zip(xs, ws_)]
+        run("c4 Llama-3-70B-shaped layer 0, scalesweep_wmse batched, dynamic S",
+            lambda: nv.quantize_batched(xs, "scalesweep_wmse", 16, weights=ws_, outs=outs))
+    if copy_calibration:     # a plain 436 MB device copy, for scaling FETCH/WRITE_SIZE
+        src = torch.empty(436207616 // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        ran.append("copy of 436207616 bytes")
+    print(json.dumps({"profile_config": name, "launches_each": reps, "ran": ran}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -238,6 +290,9 @@ def main():
     import paper_2606_07618_amd as nv
 
     dev = torch.device("cuda:0")
+    if args.profile_config:
+        profile_config(args.profile_config, nv, workloads, torch, dev, args.copy_calibration)
+        return
     layer = workloads.llama8b_layer(dev)
     names = list(layer)
     xs = [layer[n][0] for n in names]
