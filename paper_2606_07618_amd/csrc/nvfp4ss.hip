@@ -288,13 +288,14 @@ template <bool WEIGHTED, int LPB, int NC>
 __device__ __forceinline__ void significand_group_losses(const float (&y)[kLaneElems],
                                                          const float (&w)[kLaneElems],
                                                          const Scale* tab, int cb, int d,
-                                                         float (&J)[NC]) {
+                                                         float (&J)[NC], int dmin = 0) {
+    // members d + 8k below dmin are left out (and keep their J)
     constexpr int KMAX = (NC + 7) / 8;
     const float rM = tab[cb + d].rM;
     float M[KMAX], cvs[KMAX], acc0[KMAX], acc1[KMAX];
 #pragma unroll
     for (int k = 0; k < KMAX; ++k) {
-        if (d + 8 * k < NC) {
+        if (d + 8 * k < NC && d + 8 * k >= dmin) {
             M[k] = tab[cb + d + 8 * k].M;
             cvs[k] = tab[cb + d + 8 * k].cvs;
         }
@@ -308,7 +309,7 @@ __device__ __forceinline__ void significand_group_losses(const float (&y)[kLaneE
         asm volatile("" : "+v"(u0), "+v"(u1));
 #pragma unroll
         for (int k = 0; k < KMAX; ++k) {
-            if (d + 8 * k >= NC) continue;
+            if (d + 8 * k >= NC || d + 8 * k < dmin) continue;
             const uint32_t p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(any_bits(), u0, u1, cvs[k], 0);
             const float2v g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(p, cvs[k], 0);
             const float e0 = fmaf(-g.x, M[k], fabsf(y[i]));
@@ -324,7 +325,7 @@ __device__ __forceinline__ void significand_group_losses(const float (&y)[kLaneE
     }
 #pragma unroll
     for (int k = 0; k < KMAX; ++k)
-        if (d + 8 * k < NC) J[d + 8 * k] = group_sum<LPB>(acc0[k] + acc1[k]);
+        if (d + 8 * k < NC && d + 8 * k >= dmin) J[d + 8 * k] = group_sum<LPB>(acc0[k] + acc1[k]);
 }
 
 // The unweighted losses with the instruction order fixed by hand.  gfx950 issues two
@@ -1002,6 +1003,40 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
             } else {
                 J[0] = __builtin_inff();
                 significand_group_losses_sched<LPB, NC>(y, tab, cb, 8, J);   // offset 5 alone
+            }
+        } else if (!WGT && N > 16 && __all(cb >= 8)) {
+            // MSE at n = 32, 64, 128 (offsets -L..7): offsets -1..7 first (grouped by
+            // significand), then the lower candidates from the highest down, each scored only
+            // when a block of the wave may need it: the saturation bound of the n = 16 case,
+            // against the best loss scored so far.  Bound and losses are block-wide, so the
+            // lanes of a block decide alike; a skipped candidate scores +inf.
+            constexpr int DU = Win::L - 1;          // d of offset -1
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                if constexpr (NC <= 16) {
+                    if (r >= DU) significand_group_losses_sched<LPB, NC>(y, tab, cb, r, J);
+                    else if (r + 8 < NC) significand_group_losses_sched<LPB, NC>(y, tab, cb, r + 8, J);
+                } else {
+                    significand_group_losses<false, LPB, NC>(y, w, tab, cb, r, J, DU);
+                }
+            }
+            float jb = J[DU];
+#pragma unroll
+            for (int d = DU + 1; d < NC; ++d) jb = fminf(jb, J[d]);   // NaN codes past 126 drop out
+#pragma unroll
+            for (int d = DU - 1; d >= 0; --d) {
+                const float thr = fmaf(jb, kBand, jb) + kBandAbs;
+                const float e = ymax - 6.0f * e4m3_value(cb + d);   // 6 s is exact
+                if (__any(active && !(e * e > thr))) {
+                    const Scale sd = tab[cb + d];
+                    float u[kLaneElems];
+#pragma unroll
+                    for (int i = 0; i < kLaneElems; ++i) u[i] = fabsf(y[i]) * sd.rM;
+                    J[d] = group_sum<LPB>(cand_loss<false>(u, y, w, sd.cvs, sd.M));
+                    jb = fminf(jb, J[d]);
+                } else {
+                    J[d] = __builtin_inff();
+                }
             }
         } else if (__all(cb >= 8)) {
             // normal codes only: c, c+8, c+16 share the significand M and differ in 2^E

@@ -209,41 +209,77 @@ def _lower_bound_tensor(rows, seed):
     return x.astype(np.float32), w.astype(np.float32)
 
 
-@pytest.mark.parametrize("method", ["scalesweep_mse", "scalesweep_wmse"])
-def test_parity_lower_candidate_bound(nv, method):
-    """The n = 16 sweeps skip a lower window candidate when the saturated term of the block's
-    largest element already exceeds the best other loss by the re-scoring band.  WMSE: rows
-    where every block keeps all seven lower candidates (several compaction rounds per wave)
-    and rows where some do; MSE: waves that score offset -3 and waves that skip it; a ragged
-    last workgroup."""
-    x, w = _lower_bound_tensor(37, seed=11)
-    # the construction does what it says (oracle losses; the bound of a lower code c is
-    # w1 (y1 - 6 s_c)^2, compared with the best loss of the codes the kernel scores first)
+def _lower_bound_decisions(x, w, method, block):
+    """Per row (one wave of the kernels), how many (block, lower candidate) pairs the kernel
+    scores and how many lower candidates the whole wave skips, from the oracle's losses and the
+    kernel's schedule: n = 16 WMSE scores offsets -1..7 and bounds the rest against their best;
+    n = 16 MSE bounds offset -3 against offsets -2..7 except 5; n > 16 MSE scores -1..7, then
+    the lower offsets from the highest down, each when any block of the wave may need it,
+    tightening the best loss with what it scored.  The bound of a lower code c is
+    w1 (y1 - 6 s_c)^2 for the block's largest element."""
     wmse = method.endswith("wmse")
-    L = oracle.window_lower(method, 16)
-    kept_rows = {k: [] for k in range(4)}
+    L = oracle.window_lower(method, block)
+    nb = 1024 // block
+    kept, skipped = [], []
     for r in range(x.shape[0]):
-        kept = 0
-        for blk in range(64):
-            y = np.abs(x[r, 16 * blk:16 * blk + 16]).astype(np.float64)
-            wb = w[16 * blk:16 * blk + 16].astype(np.float64) if wmse else np.ones(16)
+        info = []
+        for blk in range(nb):
+            y = np.abs(x[r, block * blk:block * blk + block]).astype(np.float64)
+            wb = w[block * blk:block * blk + block].astype(np.float64) if wmse else np.ones(block)
             res = oracle.block_sweep(y, wb if wmse else None, L, 7)
-            c0 = res["c0"]
-            first = c0 - 1 if wmse else c0 - 2          # codes scored before the bound
-            jb = min(res["J"][c] for c in range(first, res["hi"] + 1) if wmse or c != c0 + 5)
+            c0, lo, hi, J = res["c0"], res["lo"], res["hi"], res["J"]
+            if block == 16 and not wmse:
+                scored = [c for c in range(c0 - 2, hi + 1) if c != c0 + 5]
+                lower = [c0 - 3] if c0 - 3 >= lo else []
+            else:
+                scored = list(range(c0 - 1, hi + 1))
+                lower = list(range(c0 - 2, lo - 1, -1))
             i1 = int(np.argmax(y))
-            for c in range(res["lo"], first):
-                e = y[i1] - 6.0 * oracle.e4m3(c)
-                kept += wb[i1] * e * e <= jb * (1 + 2.0 ** -14)
-        kept_rows[r % 4].append(int(kept))
-    if wmse:
-        assert all(k == 64 * 7 for k in kept_rows[0]), kept_rows[0]
-        others = kept_rows[1] + kept_rows[2] + kept_rows[3]
-        assert max(others) < 64 * 7 and sum(k > 64 for k in others) >= 3, kept_rows
+            info.append((min(J[c] for c in scored), lower, wb[i1] * 1.0, y[i1], J))
+        if block == 16:
+            k = 0
+            for jb, lower, w1, y1, _ in info:
+                k += sum(w1 * (y1 - 6.0 * oracle.e4m3(c)) ** 2 <= jb * (1 + 2.0 ** -14) for c in lower)
+            kept.append(k)
+            skipped.append(0)
+        else:
+            jbs = [i[0] for i in info]
+            k = sk = 0
+            for step in range(L - 1):
+                need = [step < len(lower) and (y1 - 6.0 * oracle.e4m3(lower[step])) ** 2
+                        <= jbs[b] * (1 + 2.0 ** -14) for b, (_, lower, _, y1, _) in enumerate(info)]
+                if any(need):
+                    k += sum(need)
+                    for b, (_, lower, _, _, J) in enumerate(info):
+                        if step < len(lower):
+                            jbs[b] = min(jbs[b], J[lower[step]])
+                else:
+                    sk += 1
+            kept.append(k)
+            skipped.append(sk)
+    return kept, skipped
+
+
+@pytest.mark.parametrize("method, block", [("scalesweep_mse", 16), ("scalesweep_wmse", 16),
+                                           ("scalesweep_mse", 32), ("scalesweep_mse", 64),
+                                           ("scalesweep_mse", 128)])
+def test_parity_lower_candidate_bound(nv, method, block):
+    """The sweeps skip a lower window candidate when the saturated term of the block's
+    largest element already exceeds the best loss scored so far by the re-scoring band.  WMSE
+    n = 16: rows where every block keeps all seven lower candidates (seven compaction rounds)
+    and rows where some do; MSE: waves that score a lower candidate and waves that skip it; a
+    ragged last workgroup."""
+    x, w = _lower_bound_tensor(37, seed=11)
+    kept, skipped = _lower_bound_decisions(x, w, method, block)   # the construction does what it says
+    if method.endswith("wmse"):
+        assert all(k == 64 * 7 for k in kept[0::4]), kept
+        others = [k for r, k in enumerate(kept) if r % 4]
+        assert max(others) < 64 * 7 and sum(k > 64 for k in others) >= 3, kept
+    elif block == 16:
+        assert sum(k > 0 for k in kept) >= 5 and sum(k == 0 for k in kept) >= 5, kept
     else:
-        per_row = [k for ks in kept_rows.values() for k in ks]
-        assert sum(k > 0 for k in per_row) >= 5 and sum(k == 0 for k in per_row) >= 5, kept_rows
-    check(nv, method, torch.from_numpy(x).to(DEV), 16, torch.from_numpy(w).to(DEV), static=1.0)
+        assert sum(k > 0 for k in kept) >= 5 and sum(skipped) >= 5, (kept, skipped)
+    check(nv, method, torch.from_numpy(x).to(DEV), block, torch.from_numpy(w).to(DEV), static=1.0)
 
 
 @pytest.mark.parametrize("method", METHODS)
