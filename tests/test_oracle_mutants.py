@@ -12,10 +12,12 @@ import oracle
 ROOT = Path(__file__).resolve().parents[1]
 
 # (name, original text, planted text): every original must occur exactly once.
-# Not listed: rounding s_base to the nearest instead of down inside the selection only.  It
-# moves the window up by one code exactly when max|y| / 6 lies above an FP8 midpoint; the
-# extra top code then ties at best with I(s_base^FP8) (Lemma 1), and no block with an optimum
-# at the lower edge and such a maximum was found, so its outputs match the oracle's.
+# Rounding s_base to the nearest FP8 value instead of down moves the window up by one code
+# exactly when max|y| / 6 lies above an FP8 midpoint.  For a normal base code the extra top
+# code loses to its half inside the window (Lemma 1, which needs s / 2 on the FP8 grid), but
+# for the odd subnormal codes 1..7 it does not, and tests/test_oracle_subnormal.py holds blocks
+# whose code changes; the two "nearest" mutants below plant the mistake in the selection and in
+# the window-variant path.
 MUTANTS = [
     ("fp4_tie_rule", "if (a > mid || (a == mid && ((k + 1) % 2) == 0))",
      "if (a > mid || (a == mid && ((k + 1) % 2) == 1))"),
@@ -43,6 +45,12 @@ MUTANTS = [
     ("s0_rounds_to_nearest_in_sweep",
      "double ymax = block_ymax(y, n);\n    int c0 = nvfp4_ref_floor_fp8(ymax, 6.0);",
      "double ymax = block_ymax(y, n);\n    int c0 = nvfp4_ref_nearest_fp8(ymax, 6.0);"),
+    ("s_base_nearest_in_selection",
+     "int U = nvfp4_ref_window_upper();\n    int c0 = nvfp4_ref_floor_fp8(ymax, 6.0);",
+     "int U = nvfp4_ref_window_upper();\n    int c0 = nvfp4_ref_nearest_fp8(ymax, 6.0);"),
+    ("window_base_nearest",
+     "int c0 = nvfp4_ref_floor_fp8(block_ymax(y, block), 6.0);",
+     "int c0 = nvfp4_ref_nearest_fp8(block_ymax(y, block), 6.0);"),
     ("window_not_clamped_to_1", "int lo = c0 - L < 1 ? 1 : c0 - L;\n    int hi = c0 + U > E4M3_MAX_CODE ? E4M3_MAX_CODE : c0 + U;\n    const float* wm",
      "int lo = c0 - L < 0 ? 0 : c0 - L;\n    int hi = c0 + U > E4M3_MAX_CODE ? E4M3_MAX_CODE : c0 + U;\n    const float* wm"),
     ("zero_tensor_scale", "        *S = 1.0f;\n        return REF_OK;", "        *S = 0.5f;\n        return REF_OK;"),
@@ -72,9 +80,12 @@ MUTANTS = [
 
 
 PIN_FILES = ["tests/test_oracle_pins.py", "tests/test_oracle_bruteforce.py",
+             "tests/test_oracle_subnormal.py",
              "tests/test_oracle_windows.py", "tests/test_oracle_optimum.py",
              "tests/test_oracle_online.py", "tests/test_oracle_ldlq.py"]
 PRIMARY_FILE = [("ldlq_", "tests/test_oracle_ldlq.py"),
+                ("s_base_nearest", "tests/test_oracle_subnormal.py"),
+                ("window_base_nearest", "tests/test_oracle_subnormal.py"),
                 ("online_", "tests/test_oracle_online.py"),
                 ("swizzle_", "tests/test_oracle_online.py"),
                 ("norm_", "tests/test_oracle_online.py"),
