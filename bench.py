@@ -58,9 +58,9 @@ def parse():
                          "rocprofv3 counter runs) and exit: c0 the FP32 1024x1024 matrix, c2 the "
                          "8192x8192 block-size sweep, c3 the online tensors, c4 one "
                          "Llama-3-70B-shaped layer")
-    ap.add_argument("--c4-layers", type=int, default=2,
+    ap.add_argument("--c4-layers", type=int, default=80,
                     help="Llama-3-70B-shaped layers to stream through the WMSE quantizer "
-                         "(80 is the whole model)")
+                         "(80, the default, is the whole model)")
     return ap.parse_args()
 
 
@@ -82,6 +82,32 @@ def read_traffic():
     return int(d["hbm_bytes_per_launch"])
 
 
+def read_valu():
+    """Executed VALU lane-instructions per launch of the dominant kernel (rocprofv3
+    SQ_INSTS_VALU x 64, mean over the layer's 7 tensors) from the committed counter summary, or
+    None if the counters were taken on another version of the kernel source."""
+    f = ROOT / "profiles" / "valu_scalesweep_wmse_llama8b_layer.txt"
+    if not f.exists():
+        return None
+    d = dict(line.split(None, 1) for line in f.read_text().splitlines() if line.strip())
+    if d.get("kernel_source_sha256_16", "").strip() != kernel_source_hash():
+        return None
+    return float(d["valu_lane_instructions_per_launch"])
+
+
+def host_cpu():
+    """The host CPU's model name and the cores this process may run on."""
+    model = None
+    try:
+        for line in Path("/proc/cpuinfo").read_text().splitlines():
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return model, len(os.sched_getaffinity(0))
+
+
 def _timed(torch, fn, reps):
     """Mean milliseconds of fn over reps calls, HIP events on the current stream (which the
     library launches on)."""
@@ -94,6 +120,38 @@ def _timed(torch, fn, reps):
     e1.record()
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / reps
+
+
+def _median_call(torch, fn, reps):
+    """Median milliseconds of single calls of fn (HIP events around each call on the current
+    stream), after one untimed call."""
+    fn()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for e0, e1 in ev:
+        e0.record()
+        fn()
+        e1.record()
+    torch.cuda.synchronize()
+    ts = sorted(e0.elapsed_time(e1) for e0, e1 in ev)
+    return ts[reps // 2]
+
+
+def measure_c0(nv, workloads, torch, dev):
+    """The FP32 [1024, 1024] N(0, 1) matrix (seed 0), ScaleSweep-MSE with D = 448 and a
+    dynamic S (its amax pass, scale fold and sweep), per-call latency: median of 50 calls, each
+    timed with HIP events.  At 4 MiB the call is launch-bound, so no roofline fraction."""
+    x = torch.from_numpy(workloads.c0_matrix()).to(dev)
+    ws = nv.workspace(dev)
+    out = {"workload": "fp32 [1024, 1024] N(0, 1) seed 0, block 16, D = 448, dynamic S",
+           "timing": "median of 50 single calls (HIP events)"}
+    for m in ("absmax", "scalesweep_mse"):
+        o = nv.quantize(x, m, 16, fp8_range=448.0, ws=ws)
+        us = 1e3 * _median_call(torch, lambda: nv.quantize(x, m, 16, fp8_range=448.0, ws=ws,
+                                                             out=o), 50)
+        out[m] = {"us_per_call": round(us, 2), "input_GBps": round(4 * x.numel() / us / 1e3, 1)}
+    return out
 
 
 def measure_rows(nv, workloads, torch, dev, layer):
@@ -155,14 +213,17 @@ def measure_rows(nv, workloads, torch, dev, layer):
     del x2, w2
 
     t = workloads.online_tensors(dev)
-    onl = {}
+    onl = {"timing": "median of 50 single calls (HIP events)"}
     for name in ("act", "k", "v", "q"):
         xo = t[name].reshape(-1, t[name].shape[-1])
         for m in ("absmax", "scalesweep_mse"):
-            ms = _timed(torch, lambda: nv.quantize_online(xo, m, 0.002, 16, layout="swizzled"), 10)
+            o = nv.quantize_online(xo, m, 0.002, 16, layout="swizzled")
+            ms = _median_call(torch, lambda: nv.quantize_online(xo, m, 0.002, 16, layout="swizzled",
+                                                                out=o), 50)
             onl[f"{name}_{m}"] = {"shape": list(t[name].shape), "ms": round(ms, 4),
                                   "input_GBps": round(2 * xo.numel() / ms / 1e6, 1)}
-            ms = _timed(torch, lambda: nv.quantize(xo, m, 16), 10)
+            o = nv.quantize(xo, m, 16)
+            ms = _median_call(torch, lambda: nv.quantize(xo, m, 16, out=o), 50)
             onl[f"{name}_{m}_dynamic_S"] = {"ms": round(ms, 4),
                                             "input_GBps": round(2 * xo.numel() / ms / 1e6, 1)}
     g = workloads.generator(dev, 77)
@@ -200,34 +261,63 @@ def measure_rows(nv, workloads, torch, dev, layer):
 
 
 def measure_llama70b(nv, workloads, torch, dev, layers):
-    """Llama-3-70B-shaped layers generated on the device one at a time and quantized with
-    ScaleSweep-WMSE in one batched call each (dynamic S per tensor); generation untimed.
-    Each layer's call is timed three times (HIP events around each) and the median counts, so
-    that a one-off stall of the box does not stand for a layer's cost; the slowest single
-    call is reported beside it."""
-    total_ms, elems, worst = 0.0, 0, 0.0
+    """The Llama-3-70B-shaped model streamed layer by layer: each layer's weights are generated
+    on the device (timed on the wall clock, separately), then quantized with ScaleSweep-WMSE in
+    one batched call (dynamic S per tensor), timed with HIP events around the call.  That first
+    call per layer is the streamed pass: its times summed over all layers are the model's
+    kernel time.  Two more calls per layer give a median per layer as well, so that a one-off
+    stall of the box can be told from the kernels' cost; the slowest single call is reported."""
+    stream_ms, median_ms, elems, worst = 0.0, 0.0, 0, 0.0
+    gen_s, quant_wall_s = 0.0, 0.0
+    t_all = time.perf_counter()
     for li in range(layers):
+        torch.cuda.synchronize()
+        t_g = time.perf_counter()
         lay = workloads.llama70b_layer(li, dev)
         xs = [lay[n][0] for n in lay]
         ws_ = [lay[n][1] for n in lay]
         outs = [(torch.empty((x.shape[0], x.shape[1] // 2), dtype=torch.uint8, device=dev),
                  torch.empty((x.shape[0], x.shape[1] // 16), dtype=torch.uint8, device=dev),
                  torch.empty(1, dtype=torch.float32, device=dev)) for x in xs]
+        bws = torch.empty(nv.nvfp4_batched_workspace_bytes(len(xs)) // 4, dtype=torch.int32,
+                          device=dev)
         torch.cuda.synchronize()
-        call = lambda: nv.quantize_batched(xs, "scalesweep_wmse", 16, weights=ws_, outs=outs)
-        ts = sorted(_timed(torch, call, 1) for _ in range(3))
-        total_ms += ts[1]
+        gen_s += time.perf_counter() - t_g
+        call = lambda: nv.quantize_batched(xs, "scalesweep_wmse", 16, weights=ws_, ws=bws,
+                                           outs=outs)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t_q = time.perf_counter()
+        e0.record()
+        call()
+        e1.record()
+        torch.cuda.synchronize()
+        quant_wall_s += time.perf_counter() - t_q
+        first = e0.elapsed_time(e1)
+        ts = sorted([first] + [_timed(torch, call, 1) for _ in range(2)])
+        stream_ms += first
+        median_ms += ts[1]
         worst = max(worst, ts[2])
         elems += sum(x.numel() for x in xs)
-        del lay, xs, ws_, outs
-        print(f"llama70b layer {li + 1}/{layers}: {total_ms:.1f} ms so far", file=sys.stderr,
-              flush=True)
+        del lay, xs, ws_, outs, bws
+        print(f"llama70b layer {li + 1}/{layers}: {stream_ms:.1f} ms of kernel time so far",
+              file=sys.stderr, flush=True)
+    wall_s = time.perf_counter() - t_all
     return {"workload": "Llama-3-70B-shaped decoder layers (q/o 8192^2, k/v 1024x8192, "
-                        "gate/up 28672x8192, down 8192x28672), bf16, ScaleSweep-WMSE, block 16",
-            "layers": layers, "ms_per_layer": round(total_ms / layers, 3),
-            "timing": "median of 3 calls per layer", "slowest_call_ms": round(worst, 3),
-            "input_GBps": round(2 * elems / total_ms / 1e6, 1),
-            "extrapolated_80_layers_s": round(total_ms / layers * 80 / 1e3, 2)}
+                        "gate/up 28672x8192, down 8192x28672), bf16, ScaleSweep-WMSE, block 16, "
+                        "dynamic S per tensor, weights generated per layer on the device",
+            "layers": layers, "elements": elems,
+            "kernel_ms_total": round(stream_ms, 2),
+            "input_GBps": round(2 * elems / stream_ms / 1e6, 1),
+            "ms_per_layer": round(stream_ms / layers, 3),
+            "quant_wall_s": round(quant_wall_s, 3),
+            "generation_wall_s": round(gen_s, 3),
+            "wall_s_total": round(wall_s, 3),
+            "timing": "kernel time: HIP events around the one streamed call per layer; "
+                      "quant_wall_s: host clock around those calls (launch to completion); "
+                      "wall_s_total also holds generation and the two repeat calls",
+            "median_of_3_kernel_ms_total": round(median_ms, 2),
+            "median_of_3_input_GBps": round(2 * elems / median_ms / 1e6, 1),
+            "slowest_call_ms": round(worst, 3)}
 
 
 def profile_config(name, nv, workloads, torch, dev, copy_calibration):
@@ -405,8 +495,16 @@ def main():
         "hbm_GBps_algorithmic": round(alg_bytes / avg_launch_s / 1e9, 1),
         "hbm_frac": round(alg_bytes / avg_launch_s / 1e9 / HBM_PEAK_GBS, 3),
     }
+    # executed VALU lane-instructions (counters) per launch over the same launch time: the
+    # kernel skips candidates that provably lose, so this can sit below `frac`
+    valu = read_valu()
+    roofline["executed_frac"] = (None if valu is None else
+                                 round(valu / avg_launch_s / 1e12 / VALU_PEAK_TOPS, 3))
+    roofline["executed_valu_lane_instr_per_launch"] = None if valu is None else int(valu)
 
     rows = None if args.no_rows else measure_rows(nv, workloads, torch, dev, layer)
+    if rows is not None:
+        rows["c0_fp32_1024"] = measure_c0(nv, workloads, torch, dev)
     if rows is not None and args.c4_layers > 0:
         rows["c4_llama70b_streamed"] = measure_llama70b(nv, workloads, torch, dev, args.c4_layers)
 
@@ -447,7 +545,10 @@ def main():
         # the same sample on the host's cores: the oracle's C calls release the GIL, so row
         # chunks run in parallel threads (S of each tensor's sample first, as above)
         from concurrent.futures import ThreadPoolExecutor
-        threads = max(1, min(16, os.cpu_count() or 1))
+        model, avail = host_cpu()
+        cpu["cpu_model"] = model
+        cpu["cores_available"] = avail
+        threads = max(1, min(16, avail))
         t_start = time.perf_counter()
         subs = [(xh[:rows_per], wh) for xh, wh in host]
         scales = [oracle.tensor_scale(sub, 256.0) for sub, _ in subs]

@@ -249,9 +249,10 @@ size_t nvfp4_batched_workspace_bytes(int count);
  * ascending size, each of which also reduces max |x| of the next tensor (atomic maxima into
  * that tensor's workspace), so that only the smallest reduction is not overlapped with a
  * sweep.  workspace: >= nvfp4_batched_workspace_bytes(count), 16-byte aligned, no
- * initialization; two calls in flight at the same time must not share it.  Errors as for the
- * single-tensor calls (validated for every tensor before any launch); count < 0 or an unknown
- * method: NVFP4_ERR_ARG. */
+ * initialization; two calls in flight at the same time must not share it.  The call allocates
+ * no host or device memory for any count (the ascending order is found by rescanning the
+ * descriptors).  Errors as for the single-tensor calls (validated for every tensor before any
+ * launch); count < 0 or an unknown method: NVFP4_ERR_ARG. */
 int nvfp4_quant_batched(int method, const nvfp4_tensor* tensors, int count, int dtype, int block,
                         float fp8_range, void* workspace, size_t workspace_bytes, void* stream);
 

@@ -7,6 +7,7 @@ library is not built, importing the binding raises.
 """
 from .nvfp4 import (  # noqa: F401
     LIB_PATH,
+    METHOD_IDS,
     NVFP4Error,
     block_loss,
     block_optimum,

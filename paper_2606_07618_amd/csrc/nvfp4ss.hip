@@ -39,6 +39,7 @@
 #include <math.h>
 #include <stdint.h>
 
+
 #include "nvfp4ss.h"
 
 namespace {
@@ -1396,7 +1397,9 @@ int run_quant(const Call& c) {
 // tensor of the chain into that tensor's slots, and the next kernel folds them into its S.
 // So every reduction but the smallest tensor's rides along with an arithmetic-bound sweep,
 // and no kernel sits between two sweeps.  Ascending order keeps the next tensor's share per
-// workgroup small (at most 4x its own tile for a decoder layer).
+// workgroup small (at most 4x its own tile for a decoder layer).  The chain is walked in
+// place: each step scans the list for the smallest (size, index) after the current one, so
+// the call allocates nothing for any count (count^2 comparisons on the host).
 int run_batched(int method, const nvfp4_tensor* t, int count, int dtype, int block,
                 float fp8_range, void* ws, size_t ws_bytes, hipStream_t main) {
     if (count < 0) return NVFP4_ERR_ARG;
@@ -1410,42 +1413,42 @@ int run_batched(int method, const nvfp4_tensor* t, int count, int dtype, int blo
                     fp8_range, 0.0f, t[k].tensor_scale, t[k].q, t[k].scales,
                     ws_of(k), kWorkspaceBytes, main};
     };
-    int order[256];
-    int* chain = count <= 256 ? order : new int[count];
-    int len = 0;
+    auto size_of = [&](int k) { return t[k].rows * t[k].cols; };
     for (int k = 0; k < count; ++k) {
         const int rc = validate(call_of(k));
-        if (rc != NVFP4_OK) {
-            if (chain != order) delete[] chain;
-            return rc;
+        if (rc != NVFP4_OK) return rc;
+    }
+    // the non-empty tensor that follows k in ascending (size, index) order (k < 0: the first),
+    // or -1 after the last
+    auto next_of = [&](int k) {
+        int best = -1;
+        for (int j = 0; j < count; ++j) {
+            const int64_t sj = size_of(j);
+            if (sj == 0) continue;
+            if (k >= 0 && (sj < size_of(k) || (sj == size_of(k) && j <= k))) continue;
+            if (best < 0 || sj < size_of(best)) best = j;   // ties keep the lower index
         }
-        if (t[k].rows * t[k].cols > 0) chain[len++] = k;
-    }
-    auto size_of = [&](int k) { return t[k].rows * t[k].cols; };
-    for (int a = 1; a < len; ++a) {          // stable insertion sort by size
-        const int k = chain[a];
-        int b = a;
-        for (; b > 0 && size_of(chain[b - 1]) > size_of(k); --b) chain[b] = chain[b - 1];
-        chain[b] = k;
-    }
+        return best;
+    };
     const int64_t elem_bytes = dtype == NVFP4_IN_F32 ? 4 : 2;
     bool ok = true;
     for (int k = 0; ok && k < count; ++k)
         if (size_of(k) == 0) ok = launch_empty(call_of(k), main) == hipSuccess;
+    int cur = next_of(-1);
     int npart = 0;
-    if (ok && len > 0) ok = launch_scale(call_of(chain[0]), main, &npart, ws, count) == hipSuccess;
-    for (int j = 0; ok && j < len; ++j) {
+    if (ok && cur >= 0) ok = launch_scale(call_of(cur), main, &npart, ws, count) == hipSuccess;
+    for (bool first = true; ok && cur >= 0; first = false) {
+        const int kn = next_of(cur);
         Chain ch;
-        ch.scale_src = j == 0 ? kScaleWorkspace : kScaleSlots;
-        if (j + 1 < len) {
-            const int kn = chain[j + 1];
+        ch.scale_src = first ? kScaleWorkspace : kScaleSlots;
+        if (kn >= 0) {
             ch.nx = t[kn].x;
             ch.nx_bytes = size_of(kn) * elem_bytes;
             ch.nx_ws = reinterpret_cast<uint32_t*>(ws_of(kn));
         }
-        ok = launch_main(call_of(chain[j]), main, ch) == hipSuccess;
+        ok = launch_main(call_of(cur), main, ch) == hipSuccess;
+        cur = kn;
     }
-    if (chain != order) delete[] chain;
     return ok ? NVFP4_OK : NVFP4_ERR_HIP;
 }
 
