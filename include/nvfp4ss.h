@@ -58,7 +58,8 @@ typedef enum {
     NVFP4_ERR_ARG = -5,       /* fp8_range, static_scale or a window out of range */
     NVFP4_ERR_WORKSPACE = -6, /* dynamic scale requested without a large enough workspace */
     NVFP4_ERR_ALIGN = -7,     /* x, col_weight or workspace not 16-byte aligned, q not 8 */
-    NVFP4_ERR_HIP = -8        /* a kernel launch failed */
+    NVFP4_ERR_HIP = -8,       /* a kernel launch failed */
+    NVFP4_ERR_LIMIT = -10     /* more than the no-allocation entry point's fixed scratch holds */
 } nvfp4_status;
 
 /* Bytes of device workspace the dynamic-scale path needs (a small constant, 10 KiB).
@@ -255,6 +256,23 @@ size_t nvfp4_batched_workspace_bytes(int count);
  * launch); count < 0 or an unknown method: NVFP4_ERR_ARG. */
 int nvfp4_quant_batched(int method, const nvfp4_tensor* tensors, int count, int dtype, int block,
                         float fp8_range, void* workspace, size_t workspace_bytes, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): nvfp4_quant_batched without a workspace argument.
+ * The scratch it needs (amax partials, S and 1/S, |x| maximum slots: nvfp4_workspace_bytes()
+ * per tensor) lives in a fixed device array of NVFP4_NOALLOC_MAX_TENSORS such workspaces
+ * (320 KiB) that the library defines and each GPU holds until the process ends; the call
+ * allocates nothing, host or device.  On its first call for a device it looks up that device's
+ * copy of the array (hipGetSymbolAddress; the device is the stream's, or the current one for
+ * the null stream).  Outputs are bit-identical to nvfp4_quant_batched's.  count above
+ * NVFP4_NOALLOC_MAX_TENSORS: NVFP4_ERR_LIMIT, nothing launched; other errors as for
+ * nvfp4_quant_batched.  Every call on one GPU shares that GPU's array and leaves its last
+ * contents there (the chain clears what must start at zero with a kernel of its own): calls
+ * that overlap in time on one GPU (other streams, other host threads) race and must not be
+ * issued; calls ordered on one stream are safe. */
+#define NVFP4_NOALLOC_MAX_TENSORS 32
+int nvfp4_quant_batched_noalloc(int method, const nvfp4_tensor* tensors, int count, int dtype,
+                                int block, float fp8_range, void* stream);
 
 /* Reconstruction x_hat_i = q_i * s_{block(i)} * S (NVFP4 Quantization section) into out
  * [rows, cols] binary32 (out_dtype must be NVFP4_IN_F32): q * s is exact, so each output is the

@@ -8,6 +8,7 @@ library is not built, importing the binding raises.
 from .nvfp4 import (  # noqa: F401
     LIB_PATH,
     METHOD_IDS,
+    NOALLOC_MAX_TENSORS,
     NVFP4Error,
     block_loss,
     block_optimum,
@@ -26,6 +27,7 @@ from .nvfp4 import (  # noqa: F401
     nvfp4_ldlq,
     nvfp4_ldlq_workspace_bytes,
     nvfp4_quant_batched,
+    nvfp4_quant_batched_noalloc,
     nvfp4_quant_absmax,
     nvfp4_quant_four_over_six,
     nvfp4_quant_online,

@@ -39,6 +39,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
 
 #include "nvfp4ss.h"
 
@@ -1499,7 +1500,64 @@ int run_online(const Call& c) {
 
 }  // namespace
 
+// ---------------------------------------------------------------------------------------
+// Fixed scratch of the no-allocation batched entry point.
+// ---------------------------------------------------------------------------------------
+
+namespace nvfp4ss_noalloc {
+
+constexpr int kMaxTensors = NVFP4_NOALLOC_MAX_TENSORS;
+constexpr int kMaxDevices = 64;
+
+// One workspace per tensor of a call.  On the host this name is only a stand-in for the
+// symbol: each device holds its own copy, whose address hipGetSymbolAddress returns.
+__device__ __align__(256) uint8_t scratch[kMaxTensors * kWorkspaceBytes];
+
+std::mutex lookup_mu;
+void* device_ptr[kMaxDevices];     // per device: that device's copy of `scratch`
+
+// The address of `scratch` on the device that runs `stream`, looked up once per device with
+// that device current.
+int scratch_for(hipStream_t stream, void** out) {
+    int dev = -1;
+    if (stream == nullptr) {
+        if (hipGetDevice(&dev) != hipSuccess) return NVFP4_ERR_HIP;
+    } else if (hipStreamGetDevice(stream, &dev) != hipSuccess) {
+        return NVFP4_ERR_HIP;
+    }
+    if (dev < 0 || dev >= kMaxDevices) return NVFP4_ERR_ARG;
+    std::lock_guard<std::mutex> lock(lookup_mu);
+    if (!device_ptr[dev]) {
+        int cur = -1;
+        if (hipGetDevice(&cur) != hipSuccess) return NVFP4_ERR_HIP;
+        if (cur != dev && hipSetDevice(dev) != hipSuccess) return NVFP4_ERR_HIP;
+        void* ptr = nullptr;
+        const hipError_t err = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (cur != dev) (void)hipSetDevice(cur);
+        if (err != hipSuccess || !ptr) return NVFP4_ERR_HIP;
+        device_ptr[dev] = ptr;
+    }
+    *out = device_ptr[dev];
+    return NVFP4_OK;
+}
+
+}  // namespace nvfp4ss_noalloc
+
 extern "C" {
+
+int nvfp4_quant_batched_noalloc(int method, const nvfp4_tensor* tensors, int count, int dtype,
+                                int block, float fp8_range, void* stream) {
+    if (count < 0) return NVFP4_ERR_ARG;
+    if (count > nvfp4ss_noalloc::kMaxTensors) return NVFP4_ERR_LIMIT;
+    if (count == 0) return run_batched(method, tensors, 0, dtype, block, fp8_range, nullptr, 0,
+                                       (hipStream_t)stream);
+    if (!tensors) return NVFP4_ERR_NULL;
+    void* ws = nullptr;
+    const int rc = nvfp4ss_noalloc::scratch_for((hipStream_t)stream, &ws);
+    if (rc != NVFP4_OK) return rc;
+    return run_batched(method, tensors, count, dtype, block, fp8_range, ws,
+                       (size_t)count * kWorkspaceBytes, (hipStream_t)stream);
+}
 
 int64_t nvfp4_scales_bytes(int64_t rows, int64_t cols, int block, int layout) {
     return scales_bytes(rows, cols, block, layout);
@@ -1541,6 +1599,7 @@ const char* nvfp4_status_string(int status) {
         case NVFP4_ERR_WORKSPACE: return "dynamic global scale needs a workspace of nvfp4_workspace_bytes() bytes";
         case NVFP4_ERR_ALIGN: return "misaligned pointer (x, col_weight, workspace: 16 bytes; q: 8 bytes)";
         case NVFP4_ERR_HIP: return "HIP kernel launch failed";
+        case NVFP4_ERR_LIMIT: return "more tensors than the no-allocation call's fixed scratch holds (NVFP4_NOALLOC_MAX_TENSORS)";
         default: return "unknown status";
     }
 }

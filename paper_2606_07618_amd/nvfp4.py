@@ -14,6 +14,7 @@ F32, BF16 = 0, 1
 STATUS = {
     0: "ok", -1: "null pointer", -2: "bad shape", -3: "bad block", -4: "bad dtype",
     -5: "bad argument", -6: "workspace", -7: "alignment", -8: "HIP launch failed",
+    -10: "beyond the no-allocation call's fixed scratch",
 }
 DEFAULT_RANGE = {"absmax": 448.0, "four_over_six": 256.0, "scalesweep_mse": 256.0,
                  "scalesweep_wmse": 256.0}
@@ -37,6 +38,7 @@ def _load():
         "nvfp4_workspace_bytes": (SZ, []),
         "nvfp4_batched_workspace_bytes": (SZ, [I]),
         "nvfp4_quant_batched": (I, [I, P, I, I, I, F, P, SZ, P]),
+        "nvfp4_quant_batched_noalloc": (I, [I, P, I, I, I, F, P]),
         "nvfp4_status_string": (ctypes.c_char_p, [I]),
         "nvfp4_quant_absmax": (I, quant),
         "nvfp4_quant_four_over_six": (I, quant_w),
@@ -92,6 +94,8 @@ nvfp4_ldlq_workspace_bytes = lib.nvfp4_ldlq_workspace_bytes
 nvfp4_ldlq = lib.nvfp4_ldlq
 nvfp4_batched_workspace_bytes = lib.nvfp4_batched_workspace_bytes
 nvfp4_quant_batched = lib.nvfp4_quant_batched
+nvfp4_quant_batched_noalloc = lib.nvfp4_quant_batched_noalloc
+NOALLOC_MAX_TENSORS = 32
 METHOD_IDS = {"absmax": 0, "four_over_six": 1, "scalesweep_mse": 2, "scalesweep_wmse": 3}
 
 
@@ -211,9 +215,11 @@ def quantize_window(x: torch.Tensor, block: int = 16, weight: torch.Tensor | Non
 
 def quantize_batched(xs, method: str = "scalesweep_wmse", block: int = 16, weights=None,
                      fp8_range: float | None = None, ws: torch.Tensor | None = None,
-                     outs=None):
+                     outs=None, noalloc: bool = False):
     """Quantize a list of 2-D device tensors (one dtype) with one method and a dynamic global
-    scale each, in one batched call.  Returns a list of (q, scales, S)."""
+    scale each, in one batched call.  Returns a list of (q, scales, S).  ``noalloc`` calls
+    nvfp4_quant_batched_noalloc (the library's fixed scratch, at most NOALLOC_MAX_TENSORS
+    tensors) instead of passing a workspace."""
     if not xs:
         return []
     dev = xs[0].device
@@ -231,6 +237,12 @@ def quantize_batched(xs, method: str = "scalesweep_wmse", block: int = 16, weigh
         arr[k] = NVFP4Tensor(x.data_ptr(), x.shape[0], x.shape[1],
                              None if w is None else w.data_ptr(), S.data_ptr(), q.data_ptr(),
                              sc.data_ptr())
+    if noalloc:
+        rc = nvfp4_quant_batched_noalloc(METHOD_IDS[method], ctypes.cast(arr, ctypes.c_void_p),
+                                         len(xs), dt, block, ctypes.c_float(D), _stream(dev))
+        if rc != 0:
+            raise NVFP4Error(rc, "nvfp4_quant_batched_noalloc")
+        return outs
     nbytes = nvfp4_batched_workspace_bytes(len(xs))
     if ws is None or ws.numel() * ws.element_size() < nbytes:
         ws = torch.empty(nbytes // 4, dtype=torch.int32, device=dev)
