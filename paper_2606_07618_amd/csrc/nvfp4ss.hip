@@ -290,14 +290,14 @@ template <bool WEIGHTED, int LPB, int NC>
 __device__ __forceinline__ void significand_group_losses(const float (&y)[kLaneElems],
                                                          const float (&w)[kLaneElems],
                                                          const Scale* tab, int cb, int d,
-                                                         float (&J)[NC], int dmin = 0) {
-    // members d + 8k below dmin are left out (and keep their J)
+                                                         float (&J)[NC], int dmin = 0, int dlim = NC) {
+    // members d + 8k below dmin or at dlim and above are left out (and keep their J)
     constexpr int KMAX = (NC + 7) / 8;
     const float rM = tab[cb + d].rM;
     float M[KMAX], cvs[KMAX], acc0[KMAX], acc1[KMAX];
 #pragma unroll
     for (int k = 0; k < KMAX; ++k) {
-        if (d + 8 * k < NC && d + 8 * k >= dmin) {
+        if (d + 8 * k < dlim && d + 8 * k >= dmin) {
             M[k] = tab[cb + d + 8 * k].M;
             cvs[k] = tab[cb + d + 8 * k].cvs;
         }
@@ -311,7 +311,7 @@ __device__ __forceinline__ void significand_group_losses(const float (&y)[kLaneE
         asm volatile("" : "+v"(u0), "+v"(u1));
 #pragma unroll
         for (int k = 0; k < KMAX; ++k) {
-            if (d + 8 * k >= NC || d + 8 * k < dmin) continue;
+            if (d + 8 * k >= dlim || d + 8 * k < dmin) continue;
             const uint32_t p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(any_bits(), u0, u1, cvs[k], 0);
             const float2v g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(p, cvs[k], 0);
             const float e0 = fmaf(-g.x, M[k], fabsf(y[i]));
@@ -327,7 +327,7 @@ __device__ __forceinline__ void significand_group_losses(const float (&y)[kLaneE
     }
 #pragma unroll
     for (int k = 0; k < KMAX; ++k)
-        if (d + 8 * k < NC && d + 8 * k >= dmin) J[d + 8 * k] = group_sum<LPB>(acc0[k] + acc1[k]);
+        if (d + 8 * k < dlim && d + 8 * k >= dmin) J[d + 8 * k] = group_sum<LPB>(acc0[k] + acc1[k]);
 }
 
 // The unweighted losses with the instruction order fixed by hand.  gfx950 issues two
@@ -415,11 +415,17 @@ __device__ __forceinline__ void significand_group_losses_sched(const float (&y)[
 // Weighted ScaleSweep at n = 16 with provably losing candidates skipped.
 // ---------------------------------------------------------------------------------------
 
-// The remaining (block, candidate) items of a wave, compacted candidate-major: owner lane in
-// bits 5:0, candidate code in bits 12:6; each slot then receives its item's loss.
+// The (block, candidate) items of a wave that the in-place sweep leaves to a shared pass,
+// compacted lane by lane: owner lane in bits 5:0, candidate code in bits 12:6; each slot then
+// receives its item's loss.  A lane has at most kPrunedLow + 1 items; the slots past the last
+// possible item give the last round's idle lanes somewhere to write.  Beside the list, every
+// lane's |y| (4 x 16 bytes, stored transposed: chunk k of lane L at ay[k][L], so that the
+// stores are contiguous across the wave), read back by the lanes that score its items.
 constexpr int kPrunedLow = 7;                          // candidates d < 7 (offsets -8..-2)
+constexpr int kItemSlots = 64 * (kPrunedLow + 2);      // 8 items per lane at most, + a spare round
 struct PrunedLds {
-    uint32_t item[kThreads / 64][64 * (kPrunedLow + 1)];   // one spare round for idle lanes
+    uint32_t item[kThreads / 64][kItemSlots];
+    float4 ay[kThreads / 64][4][64];
 };
 
 __device__ __forceinline__ float bperm(int src_lane, float v) {
@@ -430,86 +436,144 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
+// E4M3 value of a normal code c (8..126) from its bits, as e4m3_value without the subnormal case.
+__device__ __forceinline__ float e4m3_normal(int c) {
+    return __uint_as_float(((uint32_t)c << 20) + 0x3C000000u);
+}
+
 // Losses J[d] of the WMSE window (codes cb + d, d = 0..15, offsets -8..7; all codes normal).
 //
-// Offsets -1..7 (d = 7..15; d = 7 and 15 share the significand) are scored in place for every
-// block.  Each lower candidate d < 7 has a scale s below s0 <= max|y| / 6, so the block's
-// largest element saturates to 6 s there and its term alone, w1 (y1 - 6 s)^2, bounds the
-// candidate's loss from below.  That term is computed in the operation order the sweep uses
-// for it (e = RN(y1 - 6 s), which the sweep's fused multiply-add also yields; then
-// RN(RN(w1 e) e)), and a binary32 sum of non-negative terms accumulated with fused
-// multiply-adds is never below any one of its products, so the sweep's loss of d is >= the
-// bound.  A candidate whose bound exceeds the best in-place loss by more than the re-scoring
-// band is therefore neither the binary32 minimum nor inside the band, and skipping it leaves
-// the argmin and the band decisions exactly as with the full sweep; it scores +inf.
+// Offsets -1..6 (d = 7..14) are scored in place for every block.  The other candidates are
+// scored only where they can still be the window's argmin:
+//  * Lower candidates d < 7 (offsets -8..-2): their scale s is below s0 <= max|y| / 6, so the
+//    block's largest element saturates to 6 s and its term alone, w1 (y1 - 6 s)^2, bounds the
+//    candidate's loss from below.  That term is computed in the operation order the sweep uses
+//    for it (e = RN(y1 - 6 s), which the sweep's fused multiply-add also yields; then
+//    RN(RN(w1 e) e)), and a binary32 sum of non-negative terms accumulated with fused
+//    multiply-adds is never below any one of its products, so the sweep's loss of d is >= the
+//    bound.  The bound grows as s falls, so the candidates a block keeps are the top ones,
+//    d = 7 - k .. 6, and k comes from a three-step search.
+//  * Offset +7 (d = 15, code c0 + 7 >= 23): its half is offset -1, an E4M3 value of the window.
+//    When 3.5 s > max|y|, every element rounds at s to a point of the half scale's grid (the
+//    Block Scale Upper Bound lemma), so its exact loss is >= that of offset -1, which wins a
+//    tie as the smaller code: +7 cannot be the argmin.  Otherwise the largest element's term,
+//    formed exactly as the sweep forms it, bounds its loss as above.
+// A candidate whose bound exceeds the best in-place loss by more than the re-scoring band (or
+// that the lemma rules out) can be neither the binary32 minimum nor inside the band, nor the
+// exact argmin, so skipping it (loss +inf) leaves the argmin and the band decisions exactly as
+// with the full sweep.
 //
-// The remaining lower candidates of the wave (about 0.7 per block on Student-t weights) are
-// compacted candidate-major into one list and scored by all 64 lanes together, each lane
-// pulling its item's |y| and weights from the owner lane with ds_bpermute and leaving the loss
-// in the item's slot; a lane-local loop would cost the wave the largest count of its 64
-// blocks.  The losses are the operation sequence of cand_loss, bit-identical to in-place
-// scoring.  Called in uniform control flow with all 64 lanes of the wave running.
+// The kept items of the wave (about 50 per wave on Student-t weights: mostly one round) go into
+// one list and are scored by all 64 lanes together.  A lane takes one item, reads the owner's
+// |y| from LDS (four 16-byte loads) and the owner's weights from memory (four 16-byte loads,
+// cache hits: the owner has just loaded them), all issued at once, and leaves the loss in the
+// item's slot.  The losses are the operation sequence of cand_loss, bit-identical to in-place
+// scoring.  Called in uniform control flow with all 64 lanes of the wave running; woff is the
+// element offset of this lane's weights in colw.
 template <int NC>
 __device__ __forceinline__ void pruned_wmse_losses(const float (&y)[kLaneElems], const float (&w)[kLaneElems],
                                                    float ymax, bool active, const Scale* tab, int cb,
-                                                   float (&J)[NC], PrunedLds& lds) {
+                                                   float (&J)[NC], PrunedLds& lds, const float* colw,
+                                                   uint32_t woff) {
     static_assert(NC == 16 && kPrunedLow == 7, "window offsets -8..7");
+    constexpr int kTop = NC - 1;                     // d of offset +7
 #pragma unroll
     for (int d = kPrunedLow; d < kPrunedLow + 8; ++d) {
-        significand_group_losses<true, 1, NC>(y, w, tab, cb, d, J);
+        significand_group_losses<true, 1, NC>(y, w, tab, cb, d, J, 0, kTop);
         // finished here, before the next group's quotients are formed: one group live at a time
         asm volatile("" : "+v"(J[d]));
-        if (d + 8 < NC) asm volatile("" : "+v"(J[d + 8]));
     }
     asm volatile("" : "+v"(ymax));                  // the bounds below are formed after the sweep
     float jb = J[kPrunedLow];
 #pragma unroll
-    for (int d = kPrunedLow + 1; d < NC; ++d) jb = fminf(jb, J[d]);   // NaN codes past 126 drop out
+    for (int d = kPrunedLow + 1; d < kTop; ++d) jb = fminf(jb, J[d]);   // NaN codes past 126 drop out
     // inactive lanes (past the last block) keep nothing
     const float thr = active ? fmaf(jb, kBand, jb) + kBandAbs : -__builtin_inff();
     float w1 = 0.f;                                  // weight of an element with |y| = ymax
 #pragma unroll
     for (int i = 0; i < kLaneElems; ++i) w1 = fabsf(y[i]) == ymax ? w[i] : w1;
 
-    const int lane = threadIdx.x & 63;
-    uint32_t* items = lds.item[threadIdx.x >> 6];
-    uint64_t bal[kPrunedLow];                        // wave-uniform: which lanes keep candidate d
-    uint32_t base[kPrunedLow], total = 0u;
-#pragma unroll
-    for (int d = 0; d < kPrunedLow; ++d) {
-        const float sd = e4m3_value(cb + d);
-        const float e = ymax - 6.0f * sd;            // 6 sd is exact
+    // lower candidates: d is kept iff its bound is not above thr; kept ones are d >= dk
+    auto low_keep = [&](int d) {
+        const float e = ymax - 6.0f * e4m3_normal(cb + d);   // 6 s is exact
         const float t = w1 * e;
-        const float lb = t * e;
-        const bool keep = !(lb > thr);
-        bal[d] = __ballot(keep);
-        base[d] = total;
-        if (keep) items[total + lanes_below(bal[d])] = (uint32_t)lane | ((uint32_t)(cb + d) << 6);
-        total += (uint32_t)__popcll(bal[d]);
+        return !(t * e > thr);
+    };
+    int dk = low_keep(3) ? 0 : 4;                    // first kept d is in [dk, dk + 3]
+    dk += low_keep(dk + 1) ? 0 : 2;                  // ... in [dk, dk + 1]
+    dk += low_keep(dk) ? 0 : 1;                      // ... is dk (7: none kept)
+    const uint32_t nlow = (uint32_t)(kPrunedLow - dk);
+    // offset +7
+    bool keep_top = false;
+    {
+        const int ct = cb + kTop;
+        const Scale st = tab[ct];                    // NaN entries past code 126
+        if (ct <= 126 && !(3.5f * st.s > ymax)) {
+            const float u1 = ymax * st.rM;           // the sweep's quotient of this element
+            const float2v g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(
+                __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(any_bits(), u1, u1, st.cvs, 0), st.cvs, 0);
+            const float e = fmaf(-g.x, st.M, ymax);
+            const float t = w1 * e;
+            keep_top = !(t * e > thr);
+        }
+        keep_top = keep_top && active;
     }
+    // the lane's items: lower candidates d = 6, 5, ..., dk, then offset +7; positions in the
+    // wave's list from a prefix count over the lanes (binary digits of the counts, by ballot)
+    const int lane = threadIdx.x & 63;
+    const int wv = threadIdx.x >> 6;
+    uint32_t* items = lds.item[wv];
+    const uint64_t b0 = __ballot(nlow & 1u), b1 = __ballot(nlow & 2u), b2 = __ballot(nlow & 4u);
+    const uint64_t bt = __ballot(keep_top);
+    const uint32_t pos = lanes_below(b0) + 2u * lanes_below(b1) + 4u * lanes_below(b2) + lanes_below(bt);
+    const uint32_t total = (uint32_t)(__popcll(b0) + 2 * __popcll(b1) + 4 * __popcll(b2) + __popcll(bt));
+    const uint32_t idle = (uint32_t)(kItemSlots - 64 + lane);
+#pragma unroll
+    for (int j = 0; j < kPrunedLow; ++j)             // every lane stores (no branch)
+        items[(uint32_t)j < nlow ? pos + j : idle] = (uint32_t)lane | ((uint32_t)(cb + kPrunedLow - 1 - j) << 6);
+    items[keep_top ? pos + nlow : idle] = (uint32_t)lane | ((uint32_t)(cb + kTop) << 6);
     if (total != 0u) {                               // uniform
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            lds.ay[wv][k][lane] = make_float4(fabsf(y[4 * k]), fabsf(y[4 * k + 1]), fabsf(y[4 * k + 2]),
+                                              fabsf(y[4 * k + 3]));
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll 1
-        for (uint32_t r = 0; r < total; r += 64) {   // uniform; all lanes take part in the exchanges
+        for (uint32_t r = 0; r < total; r += 64) {   // uniform; every lane takes an item or idles
             const uint32_t pidx = r + (uint32_t)lane;
             const uint32_t it = pidx < total ? items[pidx] : 0u;
             const int owner = (int)(it & 63u);
+            const uint32_t ow = (uint32_t)__builtin_amdgcn_ds_bpermute(owner << 2, (int)woff);
             const Scale sc = tab[(int)(it >> 6)];    // code 0 (no item): NaN entries, loss unused
             float acc0 = 0.f, acc1 = 0.f;
 #pragma unroll
-            for (int i = 0; i < kLaneElems; i += 2) {
-                const float a0 = bperm(owner, fabsf(y[i])), a1 = bperm(owner, fabsf(y[i + 1]));
-                const float w0 = bperm(owner, w[i]), w1i = bperm(owner, w[i + 1]);
-                const float u0 = a0 * sc.rM, u1 = a1 * sc.rM;
-                const uint32_t pk = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(any_bits(), u0, u1, sc.cvs, 0);
-                const float2v g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pk, sc.cvs, 0);
-                const float e0 = fmaf(-g.x, sc.M, a0);
-                const float e1 = fmaf(-g.y, sc.M, a1);
-                acc0 = fmaf(w0 * e0, e0, acc0);
-                acc1 = fmaf(w1i * e1, e1, acc1);
-                if (i % 4 == 2) __builtin_amdgcn_sched_barrier(0);   // 8 exchanges in flight at most
+            for (int h = 0; h < 2; ++h) {            // two halves of 8 elements: 16 operands live
+                float a[8], wo[8];
+#pragma unroll
+                for (int k = 0; k < 2; ++k) {
+                    const float4 v = lds.ay[wv][2 * h + k][owner];
+                    a[4 * k] = v.x;
+                    a[4 * k + 1] = v.y;
+                    a[4 * k + 2] = v.z;
+                    a[4 * k + 3] = v.w;
+                    const float4 q4 = reinterpret_cast<const float4*>(colw + ow + 8 * h)[k];
+                    wo[4 * k] = q4.x;
+                    wo[4 * k + 1] = q4.y;
+                    wo[4 * k + 2] = q4.z;
+                    wo[4 * k + 3] = q4.w;
+                }
+#pragma unroll
+                for (int i = 0; i < 8; i += 2) {
+                    const float u0 = a[i] * sc.rM, u1 = a[i + 1] * sc.rM;
+                    const uint32_t pk = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(any_bits(), u0, u1, sc.cvs, 0);
+                    const float2v g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pk, sc.cvs, 0);
+                    const float e0 = fmaf(-g.x, sc.M, a[i]);
+                    const float e1 = fmaf(-g.y, sc.M, a[i + 1]);
+                    acc0 = fmaf(wo[i] * e0, e0, acc0);
+                    acc1 = fmaf(wo[i + 1] * e1, e1, acc1);
+                }
             }
             items[pidx] = __float_as_uint(acc0 + acc1);   // slots past total: idle lanes, unread
         }
@@ -519,7 +583,8 @@ __device__ __forceinline__ void pruned_wmse_losses(const float (&y)[kLaneElems],
     }
 #pragma unroll
     for (int d = 0; d < kPrunedLow; ++d)
-        J[d] = (bal[d] >> lane) & 1u ? __uint_as_float(items[base[d] + lanes_below(bal[d])]) : __builtin_inff();
+        J[d] = d >= dk ? __uint_as_float(items[pos + (uint32_t)(kPrunedLow - 1 - d)]) : __builtin_inff();
+    J[kTop] = keep_top ? __uint_as_float(items[pos + nlow]) : __builtin_inff();
 }
 
 // max(|a|, |b|, c) in one instruction (abs source modifiers); c >= 0.  The inputs come from
@@ -874,10 +939,12 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
         row = div_bpr((uint32_t)blk_c, p);
         kb = (uint32_t)blk_c - row * p.bpr;
     }
+    uint32_t woff = 0;                // element offset of this lane's weights in colw
     if (use_w) {
         const float* wrow = colw;
         if (p.wgroups > 1) wrow += (int64_t)weight_group(row, p) * p.bpr * N;
-        load_weights(wrow + (int64_t)kb * N + part * kLaneElems, w);
+        woff = (uint32_t)((wrow - colw) + (int64_t)kb * N + part * kLaneElems);
+        load_weights(colw + woff, w);
     } else {
 #pragma unroll
         for (int i = 0; i < kLaneElems; ++i) w[i] = 1.0f;
@@ -974,7 +1041,7 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
         if constexpr (WGT && N == 16) {
             __shared__ PrunedLds pl;
             if (__all(cb >= 8)) {
-                pruned_wmse_losses<NC>(y, w, ymax, active, tab, cb, J, pl);
+                pruned_wmse_losses<NC>(y, w, ymax, active, tab, cb, J, pl, colw, woff);
             } else {
 #pragma unroll
                 for (int d = 0; d < NC; ++d) {
@@ -1072,15 +1139,12 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
         int dstar = (int)(best & 0x7Fu);
         const float j1 = __uint_as_float(best & 0xFFFFFF80u);
         const float bound = fmaf(j1, kBand, j1) + kBandAbs;
-        uint64_t seen1 = 0, seen2 = 0;
+        // candidates inside the band, counted per lane (a compare and an add with carry each)
+        uint32_t inb = 0u;
 #pragma unroll
-        for (int d = 0; d < NC; ++d) {
-            const uint64_t m = __ballot(J[d] <= bound);
-            seen2 |= seen1 & m;
-            seen1 |= m;
-        }
-        const bool near = (seen2 >> lane) & 1ull;
-        if (seen2 != 0ull) {
+        for (int d = 0; d < NC; ++d) inb += J[d] <= bound ? 1u : 0u;
+        const bool near = inb >= 2u;
+        if (__any(near)) {
             if (near) {
                 // candidates in the band; two of them eight codes apart (one significand,
                 // scales s and 2s) that reconstruct every element identically have equal
@@ -1096,11 +1160,20 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
                 } else {
                     double jb = 0.0;
                     int db = -1;
+                    // the weights again, from memory: this rare path keeps no registers
+                    // occupied across the sweep
+                    float wx[kLaneElems];
+                    if (WGT) {
+                        load_weights(colw + woff, wx);
+                    } else {
+#pragma unroll
+                        for (int i = 0; i < kLaneElems; ++i) wx[i] = 1.0f;
+                    }
 #pragma unroll 1
                     for (int d = 0; d < NC; ++d) {
                         if ((inband >> d) & 1u) {
                             const Scale sd = tab[cb + d];
-                            const double jd = exact_loss<WGT, LPB>(y, w, sd, part, group_base);
+                            const double jd = exact_loss<WGT, LPB>(y, wx, sd, part, group_base);
                             if (db < 0 || jd < jb) {
                                 jb = jd;
                                 db = d;
