@@ -92,3 +92,73 @@ def test_skipping_bounded_candidates_keeps_the_argmin():
                         if c >= c0 - 1 or not w1 * (float(y[i1]) - 6.0 * oracle.e4m3(c)) ** 2 > jb]
                 best = min(kept, key=lambda c: (J[c], c))
                 assert best == res["c_win"], (n, method, best, res["c_win"])
+
+
+def _top_rule_blocks(count, seed):
+    """Blocks whose maximum sits anywhere in its FP8 interval (so that 3.5 E4M3(c0 + 7) falls on
+    either side of it), from the shapes above plus blocks near the grid of code c0 + 7."""
+    rng = np.random.default_rng(seed)
+    out = _blocks(16, count, seed)
+    for _ in range(count // 2):
+        c0 = int(rng.integers(16, 110))
+        s0 = oracle.e4m3(c0)
+        y = np.abs(rng.standard_normal(16)) * s0
+        y[0] = 6.0 * s0 * rng.uniform(1.0, oracle.e4m3(c0 + 1) / s0)
+        st = oracle.e4m3(c0 + 7)
+        snap = rng.random(16) < 0.5                        # some elements on the +7 grid
+        y[1:][snap[1:]] = st * np.array([0.5, 1, 1.5, 2, 3])[rng.integers(0, 5, snap[1:].sum())]
+        out.append(y.astype(np.float32))
+    return out
+
+
+def test_upper_lemma_rules_out_offset_seven():
+    """Block Scale Upper Bound lemma on the oracle's exact losses: where 3.5 E4M3(c0 + 7) > max|y|
+    (and c0 + 7 >= 16, so that half of it is the E4M3 value of c0 - 1), the loss of c0 + 7 is
+    never below that of c0 - 1, with either objective, so c0 + 7 is never the window argmin."""
+    rng = np.random.default_rng(41)
+    fired = equal = 0
+    for y in _top_rule_blocks(400, seed=41):
+        w = rng.uniform(0.0, 3.0, 16).astype(np.float32)
+        for wt in (None, w):
+            res = oracle.block_sweep(y, wt, 8, 7)
+            c0, J = res["c0"], res["J"]
+            ct = c0 + 7
+            if ct > 126 or ct < 16:
+                continue
+            assert oracle.e4m3(ct - 8) * 2.0 == oracle.e4m3(ct)
+            if 3.5 * oracle.e4m3(ct) > float(np.max(y)):
+                fired += 1
+                equal += J[ct] == J[ct - 8]
+                assert J[ct] >= J[ct - 8], (c0, J[ct], J[ct - 8])
+                assert res["c_win"] != ct
+    assert fired > 200, fired
+
+
+def test_wmse_schedule_keeps_the_argmin():
+    """Replays the WMSE n = 16 schedule of the GPU sweep on the oracle's exact losses:
+    offsets -1..6 scored; lower offsets kept as the contiguous top range whose saturation bound
+    is not above the best scored loss; offset +7 ruled out by the lemma where 3.5 s > max|y|,
+    else kept unless the largest element's term exceeds the best scored loss.  The argmin over
+    the kept candidates (smallest code on ties) is the window argmin."""
+    rng = np.random.default_rng(43)
+    for y in _top_rule_blocks(300, seed=43):
+        w = rng.uniform(0.0, 3.0, 16).astype(np.float32)
+        res = oracle.block_sweep(y, w, 8, 7)
+        c0, lo, hi, J = res["c0"], res["lo"], res["hi"], res["J"]
+        if c0 - 8 < 8 or c0 + 7 > 126:
+            continue                                      # the GPU sweeps such waves in full
+        i1 = int(np.argmax(y))
+        y1, w1 = float(y[i1]), float(w[i1])
+        scored = list(range(c0 - 1, c0 + 7))
+        jb = min(J[c] for c in scored)
+        low = [c for c in range(c0 - 8, c0 - 1) if not w1 * (y1 - 6.0 * oracle.e4m3(c)) ** 2 > jb]
+        assert low == list(range(c0 - 1 - len(low), c0 - 1))     # a contiguous top range
+        ct = c0 + 7
+        st = oracle.e4m3(ct)
+        top = []
+        if not 3.5 * st > y1:
+            g = oracle.e2m1(oracle.round_fp4(y1, st))
+            if not w1 * (y1 - g * st) ** 2 > jb:
+                top = [ct]
+        best = min(scored + low + top, key=lambda c: (J[c], c))
+        assert best == res["c_win"], (c0, best, res["c_win"])

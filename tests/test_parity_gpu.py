@@ -212,7 +212,8 @@ def _lower_bound_tensor(rows, seed):
 def _lower_bound_decisions(x, w, method, block):
     """Per row (one wave of the kernels), how many (block, lower candidate) pairs the kernel
     scores and how many lower candidates the whole wave skips, from the oracle's losses and the
-    kernel's schedule: n = 16 WMSE scores offsets -1..7 and bounds the rest against their best;
+    kernel's schedule: n = 16 WMSE scores offsets -1..6 and bounds the lower ones against their
+    best (offset +7 has a rule of its own, test_parity_offset_seven_rule);
     n = 16 MSE bounds offset -3 against offsets -2..7 except 5; n > 16 MSE scores -1..7, then
     the lower offsets from the highest down, each when any block of the wave may need it,
     tightening the best loss with what it scored.  The bound of a lower code c is
@@ -231,6 +232,9 @@ def _lower_bound_decisions(x, w, method, block):
             if block == 16 and not wmse:
                 scored = [c for c in range(c0 - 2, hi + 1) if c != c0 + 5]
                 lower = [c0 - 3] if c0 - 3 >= lo else []
+            elif block == 16:
+                scored = list(range(c0 - 1, min(c0 + 6, hi) + 1))
+                lower = list(range(c0 - 2, lo - 1, -1))
             else:
                 scored = list(range(c0 - 1, hi + 1))
                 lower = list(range(c0 - 2, lo - 1, -1))
@@ -280,6 +284,51 @@ def test_parity_lower_candidate_bound(nv, method, block):
     else:
         assert sum(k > 0 for k in kept) >= 5 and sum(skipped) >= 5, (kept, skipped)
     check(nv, method, torch.from_numpy(x).to(DEV), block, torch.from_numpy(w).to(DEV), static=1.0)
+
+
+def _offset_seven_tensor(rows, seed):
+    """[rows, 1024] binary32 for S = 1 (one 64-block row per wave), WMSE weights, built around
+    the rule for offset +7 of the n = 16 WMSE sweep.  Every block has base code c0 with mantissa
+    field 0, its other elements near the grid of code c0 + 7 (s7 = 15/8 s0), and its largest
+    element, whose weight is small, at one of: below 3.5 s7 (the upper-bound lemma rules +7
+    out), exactly 3.5 s7 (the lemma does not apply: +7 is bounded by that element's term), or
+    above it (bounded; with the others on the grid of s7, +7 often wins)."""
+    rng = np.random.default_rng(seed)
+    x = np.zeros((rows, 1024), np.float64)
+    w = rng.uniform(0.5, 2.0, 1024)
+    w[::16] = rng.uniform(0.0, 0.02, 64)                 # the largest element sits in column 0
+    E = [oracle.e4m3(c) for c in range(127)]
+    for r in range(rows):
+        for b in range(64):
+            c0 = 8 * int(rng.integers(3, 14))            # mantissa field 0
+            s0, s7 = E[c0], E[c0 + 7]
+            grid = np.array([0.5, 1.0, 1.5, 2.0, 3.0]) * s7
+            v = grid[rng.integers(0, 5, 16)] * (1.0 + rng.normal(0.0, 0.002 * (r % 3), 16))
+            kind = (r + b) % 3
+            top = (3.5 * s7 * (1.0 - 2.0 ** -12 * rng.integers(1, 64)) if kind == 0 else
+                   3.5 * s7 if kind == 1 else rng.uniform(3.5 * s7, 6.74 * s0))
+            v[0] = max(top, 6.0 * s0)                    # keeps the base code at c0
+            v = np.minimum(v, v[0])
+            x[r, 16 * b:16 * b + 16] = v * np.where(rng.random(16) < 0.5, -1.0, 1.0)
+    return x.astype(np.float32), w.astype(np.float32)
+
+
+def test_parity_offset_seven_rule(nv):
+    """WMSE n = 16: offset +7 ruled out by the upper-bound lemma, bounded at the lemma's edge,
+    and winning the window; the oracle confirms that the construction covers each case."""
+    x, w = _offset_seven_tensor(24, seed=17)
+    ruled = edge = wins = 0
+    for r in range(x.shape[0]):
+        for b in range(64):
+            y = np.abs(x[r, 16 * b:16 * b + 16])
+            res = oracle.block_sweep(y, w[16 * b:16 * b + 16], 8, 7)
+            s7 = oracle.e4m3(res["c0"] + 7)
+            ruled += 3.5 * s7 > y.max()
+            edge += 3.5 * s7 == y.max()
+            wins += res["c_win"] == res["c0"] + 7
+    assert ruled > 200 and edge > 200 and wins > 20, (ruled, edge, wins)
+    check(nv, "scalesweep_wmse", torch.from_numpy(x).to(DEV), 16, torch.from_numpy(w).to(DEV),
+          static=1.0)
 
 
 @pytest.mark.parametrize("method", METHODS)
