@@ -790,6 +790,19 @@ __device__ __forceinline__ uint32_t swizzled_offset(uint32_t m, uint32_t k, uint
     return ((m >> 7) * kt + (k >> 2)) * 512u + (m & 31u) * 16u + ((m >> 5) & 3u) * 4u + (k & 3u);
 }
 
+// Workgroups are dispatched to the 8 XCDs of the GPU round-robin (workgroup i to XCD i mod 8),
+// and each XCD has its own L2.  This regrouping gives the workgroups of XCD x a contiguous
+// eighth of the tiles (rows), so every workgroup that writes into one 512-byte scale tile of the
+// swizzled layout (128 rows) runs on the same XCD: that L2 merges their 4-byte pieces into whole
+// lines before they go to memory, instead of eight L2s writing partial lines.  Any grid size;
+// a bijection on 0..grid-1.
+constexpr uint32_t kXcds = 8;
+__device__ __forceinline__ uint32_t xcd_tile(uint32_t i, uint32_t grid) {
+    const uint32_t x = i % kXcds, j = i / kXcds;
+    const uint32_t q = grid / kXcds, r = grid % kXcds;
+    return x * q + min(x, r) + j;
+}
+
 template <int METHOD, int N>
 struct Window {
     static constexpr int L = METHOD == kSweepMse
@@ -920,7 +933,8 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
     constexpr bool WEIGHTED_OBJ = METHOD == kSweepWmse || METHOD == kFourSix || METHOD == kWindowWmse;
     __shared__ Scale tab_all[kTabSize];
     Scale* tab = tab_all + kTabLo;                 // tab[c] for codes c in -16..143
-    const uint32_t tile = blockIdx.x;                 // the workgroup's tile of this tensor
+    // the workgroup's tile of this tensor; with swizzled scales, tiles are regrouped by XCD
+    const uint32_t tile = p.swizzled ? xcd_tile(blockIdx.x, gridDim.x) : blockIdx.x;
     const int lane = threadIdx.x & 63;
     const int64_t gtid = (int64_t)tile * kThreads + threadIdx.x;
     const int64_t blk = gtid / LPB;
@@ -1212,9 +1226,12 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
         pv.x = packed[0];
         pv.y = packed[1];
         __builtin_nontemporal_store(pv, reinterpret_cast<u32x2*>(dst));
-        if (part == 0)
-            __builtin_nontemporal_store((uint8_t)code,
-                                        scales + (p.swizzled ? (int64_t)swizzled_offset(row, kb, p.sw_kt) : blk));
+        if (part == 0) {
+            if (p.swizzled)      // through L2, which merges the 4-byte pieces of a tile's lines
+                scales[swizzled_offset(row, kb, p.sw_kt)] = (uint8_t)code;
+            else
+                __builtin_nontemporal_store((uint8_t)code, scales + blk);
+        }
     }
     }
 }
