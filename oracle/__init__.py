@@ -84,6 +84,8 @@ def _bind(lib):
         "nvfp4_ref_scales_bytes": (I64, [I64, I64, I, I]),
         "nvfp4_ref_quant_online": (I, [I, P, I, I64, I64, I, P, I64, I64, F, I, P, P, P]),
         "nvfp4_ref_channel_sq_norms": (I, [P, I, I64, I64, I64, I64, I64, I64, P]),
+        "nvfp4_ref_swiglu_exp": (ctypes.c_float, [ctypes.c_float]),
+        "nvfp4_ref_swiglu": (I, [P, P, I64, P]),
         "nvfp4_ref_ldlq_order": (I, [P, I64, P]),
         "nvfp4_ref_ldlq_factor": (I, [P, I64, D, P, P, P]),
         "nvfp4_ref_ldlq": (I, [P, I, I64, I64, I, P, P, F, D, P]),
@@ -367,6 +369,24 @@ def quantize_online(method: str | int, x, static_scale: float, block: int = 16,
     if layout == "row_major":
         sc = sc.reshape(rows, cols // block)
     return q, sc
+
+
+def swiglu_exp(x: float) -> float:
+    return _load().nvfp4_ref_swiglu_exp(float(x))
+
+
+def swiglu(gate: np.ndarray, up: np.ndarray) -> np.ndarray:
+    """bfloat16 bit patterns h = bf16(silu(gate) * up) of two bfloat16 (uint16 bit pattern)
+    arrays of one shape."""
+    g = np.ascontiguousarray(gate, dtype=np.uint16)
+    u = np.ascontiguousarray(up, dtype=np.uint16)
+    if g.shape != u.shape:
+        raise ValueError("gate and up must have one shape")
+    h = np.zeros(g.shape, dtype=np.uint16)
+    rc = _load().nvfp4_ref_swiglu(_ptr(g), _ptr(u), g.size, _ptr(h))
+    if rc:
+        raise OracleError(rc, "swiglu")
+    return h
 
 
 def channel_sq_norms(x, group_rows: int = 1, groups: int = 1, group_div: int = 1,

@@ -513,6 +513,76 @@ int nvfp4_ref_quant_online(int method, const void* x, int dtype, int64_t rows, i
     return rc;
 }
 
+/* ------------------------------------------------------------------------------------- */
+/* A producer for the fused online quantizer: the SwiGLU product of a Llama MLP.           */
+/* ------------------------------------------------------------------------------------- */
+
+/* reading: the paper leaves the producer of a fused quantizer open (Overhead Analysis: the
+ * operators are memory-bound, fusion is the next step).  The product silu(g) * u of a
+ * SwiGLU MLP, the input of its down projection, is taken, with its binary32 arithmetic fixed
+ * so that a plain implementation reproduces it bit for bit:
+ *   e^x: zero below x = -80 (then 1 + e^x rounds to 1 anyway) and +inf from x = 89; else
+ *        n = rint(RN(x * RN(log2 e))), the reduced argument r = x - n ln2 with ln2 split as
+ *        0.693145751953125 + RN(ln2 - 0.693145751953125) (two fused multiply-adds), the
+ *        Taylor polynomial of degree 6 with coefficients RN(1/k!) in Horner form (fused
+ *        multiply-adds), times 2^n (exact: the result stays normal);
+ *   silu(g) = RN(g / RN(1 + e^-g)) (a correctly rounded division); h = RN(silu(g) * u),
+ *   rounded to nearest even onto bfloat16. */
+float nvfp4_ref_swiglu_exp(float x)
+{
+    if (x < -80.0f) return 0.0f;
+    if (x >= 89.0f) return INFINITY;
+    const float log2e = 1.44269502162933349609375f;          /* RN32(1 / ln 2) */
+    const float ln2_hi = 0.693145751953125f;
+    const float ln2_lo = (float)(0.6931471805599453094 - 0.693145751953125);
+    float t = x * log2e;
+    float n = rintf(t);
+    float r = fmaf(-n, ln2_hi, x);
+    r = fmaf(-n, ln2_lo, r);
+    float c[7];
+    double f = 1.0;
+    for (int k = 0; k < 7; ++k) {
+        if (k > 0) f *= (double)k;
+        c[k] = (float)(1.0 / f);                               /* RN32(1 / k!) */
+    }
+    float p = c[6];
+    for (int k = 5; k >= 0; --k) p = fmaf(p, r, c[k]);
+    return ldexpf(p, (int)n);
+}
+
+static uint16_t bf16_round(float v)
+{
+    uint32_t b;
+    memcpy(&b, &v, 4);
+    /* round to nearest even at bit 16 (finite values and infinities) */
+    uint32_t r = b + 0x7FFFu + ((b >> 16) & 1u);
+    return (uint16_t)(r >> 16);
+}
+
+static float bf16_value(uint16_t h)
+{
+    uint32_t b = (uint32_t)h << 16;
+    float v;
+    memcpy(&v, &b, 4);
+    return v;
+}
+
+/* h = bf16(RN(silu(g) * u)) elementwise over bfloat16 gate and up (count elements). */
+int nvfp4_ref_swiglu(const uint16_t* gate, const uint16_t* up, int64_t count, uint16_t* h)
+{
+    if (count < 0) return REF_ERR_SHAPE;
+    if (count > 0 && (!gate || !up || !h)) return REF_ERR_NULL;
+    for (int64_t i = 0; i < count; ++i) {
+        float g = bf16_value(gate[i]), u = bf16_value(up[i]);
+        if (!isfinite(g) || !isfinite(u)) return REF_ERR_NONFINITE;
+        float e = nvfp4_ref_swiglu_exp(-g);
+        float d = 1.0f + e;
+        float sg = g / d;
+        h[i] = bf16_round(sg * u);
+    }
+    return REF_OK;
+}
+
 /* Squared norms of the input channels (the importance scores of the WMSE section): for a
  * matrix x [rows, cols], out[g][c] = sum over the rows r of group g of x[r][c]^2, where row
  * r belongs to group ((r / group_rows) mod groups) / group_div, summed in row order in

@@ -91,6 +91,10 @@ int nvfp4_ref_quant_online(int method, const void* x, int dtype, int64_t rows, i
                            int block, const float* importance, int64_t imp_groups,
                            int64_t imp_group_rows, float static_scale, int layout,
                            float* tensor_scale, uint8_t* q, uint8_t* scales);
+/* SwiGLU producer of the fused online quantizer: e^x as specified in nvfp4_oracle.c, and
+ * h = bf16(RN(silu(g) * u)) over bfloat16 bit patterns; non-finite inputs: REF_ERR_NONFINITE. */
+float nvfp4_ref_swiglu_exp(float x);
+int nvfp4_ref_swiglu(const uint16_t* gate, const uint16_t* up, int64_t count, uint16_t* h);
 int nvfp4_ref_channel_sq_norms(const void* x, int dtype, int64_t rows, int64_t cols,
                                int64_t group_rows, int64_t groups, int64_t group_div,
                                int64_t rep_out, float* out);

@@ -74,17 +74,22 @@ MUTANTS = [
      "double lambda = 0.0 * damp * tr;"),
     ("ldlq_feedback_sign", "for (int64_t b = 0; b < a; ++b) x = x + e[b] * U[b * n + a];",
      "for (int64_t b = 0; b < a; ++b) x = x - e[b] * U[b * n + a];"),
+    ("swiglu_exp_of_plus_g", "float e = nvfp4_ref_swiglu_exp(-g);", "float e = nvfp4_ref_swiglu_exp(g);"),
+    ("swiglu_ln2_lo_dropped", "    r = fmaf(-n, ln2_lo, r);\n", "    r = fmaf(-n, 0.0f, r);\n"),
+    ("swiglu_degree_5", "    float p = c[6];\n", "    float p = 0.0f;\n"),
+    ("swiglu_bf16_truncates", "uint32_t r = b + 0x7FFFu + ((b >> 16) & 1u);", "uint32_t r = b;"),
     ("fp8_opt_ceil_not_taken", "if (nvfp4_ref_e4m3(cf) < s_opt && cf < E4M3_MAX_CODE) cc = cf + 1;",
      "if (nvfp4_ref_e4m3(cf) < s_opt && cf < E4M3_MAX_CODE) cc = cf;"),
 ]
 
 
 PIN_FILES = ["tests/test_oracle_pins.py", "tests/test_oracle_bruteforce.py",
-             "tests/test_oracle_subnormal.py",
+             "tests/test_oracle_subnormal.py", "tests/test_oracle_swiglu.py",
              "tests/test_oracle_windows.py", "tests/test_oracle_optimum.py",
              "tests/test_oracle_online.py", "tests/test_oracle_ldlq.py"]
 PRIMARY_FILE = [("ldlq_", "tests/test_oracle_ldlq.py"),
                 ("s_base_nearest", "tests/test_oracle_subnormal.py"),
+                ("swiglu_", "tests/test_oracle_swiglu.py"),
                 ("window_base_nearest", "tests/test_oracle_subnormal.py"),
                 ("online_", "tests/test_oracle_online.py"),
                 ("swizzle_", "tests/test_oracle_online.py"),
