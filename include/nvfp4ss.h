@@ -185,6 +185,26 @@ int nvfp4_quant_online(int method, const void* x, int dtype, int64_t rows, int64
                        float static_scale, int scale_layout, float* tensor_scale, uint8_t* q,
                        uint8_t* scales, void* stream);
 
+/* The producer of a quantized activation fused with its quantizer (the Overhead Analysis:
+ * the operators are memory-bound and open to fusion).  The producer is the SwiGLU product of
+ * a Llama MLP, the input of its down projection: over bfloat16 gate and up [rows, cols],
+ *   h = bf16(RN(silu(g) * u)),  silu(g) = RN(g / RN(1 + e^-g)) (a correctly rounded division),
+ * with e^x computed as: 0 for x < -80, +inf for x >= 89, otherwise n = rint(RN(x * RN32(1/ln 2))),
+ * r = fma(-n, 0.693145751953125, x), r = fma(-n, RN32(ln 2 - 0.693145751953125), r), the
+ * degree-6 Taylor polynomial in r with coefficients RN32(1/k!) in Horner form (fused
+ * multiply-adds), times 2^n; bfloat16 rounding to nearest even.
+ * nvfp4_swiglu writes h [rows, cols] (bfloat16; the unfused producer).
+ * nvfp4_quant_online_swiglu quantizes h without writing it: it equals nvfp4_swiglu followed by
+ * nvfp4_quant_online on h with dtype NVFP4_IN_BF16 and block 16 (same arguments otherwise),
+ * bit for bit, and reads 4 bytes per element instead of 8 (4 + 2 + 2).  gate, up: 16-byte
+ * aligned device pointers; cols % 16 == 0; non-finite inputs give unspecified outputs.  Errors
+ * as nvfp4_quant_online (up NULL: NVFP4_ERR_NULL). */
+int nvfp4_swiglu(const void* gate, const void* up, int64_t rows, int64_t cols, void* h, void* stream);
+int nvfp4_quant_online_swiglu(int method, const void* gate, const void* up, int64_t rows, int64_t cols,
+                              const float* importance, int64_t imp_groups, int64_t imp_group_rows,
+                              float static_scale, int scale_layout, float* tensor_scale, uint8_t* q,
+                              uint8_t* scales, void* stream);
+
 /* Importance vectors (WMSE section): squared norms of input channels.  For x [rows, cols]
  * (binary32 or bfloat16), out[g][c] = sum of x[r][c]^2 over the rows r of group
  * g = ((r / group_rows) mod groups) / group_div, accumulated in binary64 and rounded once to

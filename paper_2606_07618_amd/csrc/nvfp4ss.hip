@@ -246,6 +246,49 @@ __device__ __forceinline__ void load_weights(const float* p, float (&w)[kLaneEle
 }
 
 // ---------------------------------------------------------------------------------------
+// SwiGLU producer of the fused online quantizer: h = bf16(RN(silu(g) * u)).
+// ---------------------------------------------------------------------------------------
+
+// e^x in binary32 with every step fixed, so that a plain implementation reproduces it bit for
+// bit: 0 below -80 (1 + e^x then rounds to 1 anyway), +inf from 89; otherwise Cody-Waite
+// reduction x = n ln2 + r (ln2 as 0.693145751953125 plus the rounded rest, two fused
+// multiply-adds), the degree-6 Taylor polynomial with coefficients RN32(1/k!) in Horner form,
+// and the exact scaling by 2^n (the result is normal for x >= -80).  At most ~4 ulps from e^x.
+__device__ __forceinline__ float swiglu_exp(float x) {
+    if (x < -80.0f) return 0.0f;
+    if (x >= 89.0f) return __builtin_inff();
+    const float n = __builtin_rintf(x * 0x1.715476p+0f);   // RN32(1 / ln 2)
+    float r = fmaf(-n, 0x1.62e4p-1f, x);
+    r = fmaf(-n, 0x1.7f7d1cp-20f, r);                      // RN32(ln 2 - 0.693145751953125)
+    float q = 0x1.6c16c2p-10f;                             // 1/720
+    q = fmaf(q, r, 0x1.111112p-7f);                        // 1/120
+    q = fmaf(q, r, 0x1.555556p-5f);                        // 1/24
+    q = fmaf(q, r, 0x1.555556p-3f);                        // 1/6
+    q = fmaf(q, r, 0.5f);
+    q = fmaf(q, r, 1.0f);
+    q = fmaf(q, r, 1.0f);
+    return ldexpf(q, (int)n);
+}
+
+// The bfloat16 bit pattern (round to nearest even) of silu(g) * u = RN(RN(g / RN(1 + e^-g)) u),
+// with a correctly rounded division.  Finite inputs.
+__device__ __forceinline__ uint32_t swiglu_bf16(float g, float u) {
+    const float d = 1.0f + swiglu_exp(-g);
+    const float h = __fdiv_rn(g, d) * u;
+    const uint32_t b = __float_as_uint(h);
+    return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+}
+
+// The 16 producer outputs of one lane (bfloat16 values widened to binary32, exactly).
+__device__ __forceinline__ void swiglu_lane(const uint16_t* gate, const uint16_t* up, float (&h)[kLaneElems]) {
+    float g[kLaneElems], u[kLaneElems];
+    Loader<uint16_t>::load(gate, g);
+    Loader<uint16_t>::load(up, u);
+#pragma unroll
+    for (int i = 0; i < kLaneElems; ++i) h[i] = __uint_as_float(swiglu_bf16(g[i], u[i]) << 16);
+}
+
+// ---------------------------------------------------------------------------------------
 // Block loss of one candidate scale, binary32 (fast screen).
 // ---------------------------------------------------------------------------------------
 
@@ -760,6 +803,7 @@ struct Params {
     int win_tight;            // window variants: per-mantissa offsets (else win_lo..win_hi)
     int win_lo, win_hi;
     int swizzled;             // scales in 128 x 4 tiles (else row-major)
+    const uint16_t* up;       // fused SwiGLU input: x is the gate, this the up projection
     uint32_t sw_kt;           // 4-column scale tiles per tile row
     uint32_t wgroups;         // importance vectors: row r uses ((r / wg_rows) mod wgroups)
     uint32_t wgr_magic, wgr_shift, wgn_magic, wgn_shift;   // dividers by wg_rows, wgroups
@@ -924,7 +968,7 @@ __device__ __forceinline__ void raise_next_slot(const Params& p, uint32_t tile, 
                                m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <int METHOD, typename In, int N>
+template <int METHOD, typename In, int N, bool SWIGLU = false>
 __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ x,
                                                          const float* __restrict__ colw,
                                                          uint8_t* __restrict__ q,
@@ -945,7 +989,12 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
 
     // The tile's loads go out first; the table fill and the global-scale fold overlap them.
     float y[kLaneElems];
-    Loader<In>::load(x + blk_c * N + part * kLaneElems, y);
+    if constexpr (SWIGLU) {           // the tensor is the producer's output, formed here
+        static_assert(N == 16, "fused producer at block 16");
+        swiglu_lane(reinterpret_cast<const uint16_t*>(x) + blk_c * N, p.up + blk_c * N, y);
+    } else {
+        Loader<In>::load(x + blk_c * N + part * kLaneElems, y);
+    }
     float w[kLaneElems];
     const bool use_w = WEIGHTED_OBJ && colw != nullptr;
     uint32_t row = 0, kb = 0;         // the block's row and block column
@@ -1298,6 +1347,23 @@ __global__ __launch_bounds__(kThreads) void dequant_kernel(const uint8_t* __rest
     }
 }
 
+// The SwiGLU producer alone (the unfused path): h = bf16(silu(gate) * up), 16 elements per
+// lane, two 16-byte stores per lane.
+__global__ __launch_bounds__(kThreads) void swiglu_kernel(const uint16_t* __restrict__ gate,
+                                                          const uint16_t* __restrict__ up, int64_t n,
+                                                          uint16_t* __restrict__ h) {
+    const int64_t e = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kLaneElems;
+    if (e >= n) return;                               // n is a multiple of 16
+    float v[kLaneElems];
+    swiglu_lane(gate + e, up + e, v);
+    uint32_t w[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) w[j] = (__float_as_uint(v[2 * j]) >> 16) | (__float_as_uint(v[2 * j + 1]) & 0xFFFF0000u);
+    uint4* dst = reinterpret_cast<uint4*>(h + e);
+    dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
+    dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
+}
+
 // ---------------------------------------------------------------------------------------
 // Host side.
 // ---------------------------------------------------------------------------------------
@@ -1332,6 +1398,7 @@ struct Call {
     int win_mode = 0, win_lo = 0, win_hi = 0;     // window variants only
     int layout = NVFP4_SCALES_ROW_MAJOR;          // online calls only
     int64_t wgroups = 1, wgroup_rows = 1;
+    const void* up = nullptr;                     // fused SwiGLU calls: x is the gate
 };
 
 // Workgroups of the quantization kernel: one lane per 16 elements, one workgroup per tile.
@@ -1340,11 +1407,11 @@ int64_t quant_grid(const Call& c) {
     return (lanes + kThreads - 1) / kThreads;
 }
 
-template <int METHOD, typename In, int N>
+template <int METHOD, typename In, int N, bool SWIGLU = false>
 hipError_t launch_quant(const Call& c, const Params& p) {
     const int64_t grid = quant_grid(c);
-    hipLaunchKernelGGL((quant_kernel<METHOD, In, N>), dim3((unsigned)grid), dim3(kThreads), 0, c.stream,
-                       static_cast<const In*>(c.x), c.colw, c.q, c.scales, p);
+    hipLaunchKernelGGL((quant_kernel<METHOD, In, N, SWIGLU>), dim3((unsigned)grid), dim3(kThreads), 0,
+                       c.stream, static_cast<const In*>(c.x), c.colw, c.q, c.scales, p);
     return hipGetLastError();
 }
 
@@ -1454,8 +1521,17 @@ hipError_t launch_main(const Call& c, hipStream_t stream, const Chain& chain = C
     p.win_tight = c.win_mode == NVFP4_WINDOW_TIGHT ? 1 : 0;
     p.win_lo = c.win_lo;
     p.win_hi = c.win_hi;
+    p.up = static_cast<const uint16_t*>(c.up);
     Call cs = c;
     cs.stream = stream;
+    if (c.up) {                       // fused SwiGLU producer: bfloat16, block 16
+        switch (c.method) {
+            case kAbsMax: return launch_quant<kAbsMax, uint16_t, 16, true>(cs, p);
+            case kFourSix: return launch_quant<kFourSix, uint16_t, 16, true>(cs, p);
+            case kSweepMse: return launch_quant<kSweepMse, uint16_t, 16, true>(cs, p);
+            default: return launch_quant<kSweepWmse, uint16_t, 16, true>(cs, p);
+        }
+    }
     switch (c.method) {
         case kAbsMax: return launch_quant_m<kAbsMax>(cs, p);
         case kFourSix: return launch_quant_m<kFourSix>(cs, p);
@@ -1664,6 +1740,36 @@ int nvfp4_quant_online(int method, const void* x, int dtype, int64_t rows, int64
     c.wgroups = imp_groups;
     c.wgroup_rows = imp_group_rows;
     return run_online(c);
+}
+
+int nvfp4_quant_online_swiglu(int method, const void* gate, const void* up, int64_t rows, int64_t cols,
+                              const float* importance, int64_t imp_groups, int64_t imp_group_rows,
+                              float static_scale, int scale_layout, float* tensor_scale, uint8_t* q,
+                              uint8_t* scales, void* stream) {
+    if (!up && rows * cols > 0) return NVFP4_ERR_NULL;
+    if (rows * cols > 0 && !aligned(up, 16)) return NVFP4_ERR_ALIGN;
+    Call c{method, gate, NVFP4_IN_BF16, rows, cols, 16,
+           (method == kSweepWmse || method == kFourSix) ? importance : nullptr, 448.0f,
+           static_scale, tensor_scale, q, scales, nullptr, 0, (hipStream_t)stream};
+    c.layout = scale_layout;
+    c.wgroups = imp_groups;
+    c.wgroup_rows = imp_group_rows;
+    c.up = up;
+    return run_online(c);
+}
+
+int nvfp4_swiglu(const void* gate, const void* up, int64_t rows, int64_t cols, void* h, void* stream) {
+    if (rows < 0 || cols < 0 || cols % 16 != 0) return NVFP4_ERR_SHAPE;
+    const int64_t n = rows * cols;
+    if (n == 0) return NVFP4_OK;
+    if (!gate || !up || !h) return NVFP4_ERR_NULL;
+    if (!aligned(gate, 16) || !aligned(up, 16) || !aligned(h, 16)) return NVFP4_ERR_ALIGN;
+    const int64_t grid = (n / kLaneElems + kThreads - 1) / kThreads;
+    if (grid > 0x7FFFFFFFLL) return NVFP4_ERR_SHAPE;
+    hipLaunchKernelGGL(swiglu_kernel, dim3((unsigned)grid), dim3(kThreads), 0, (hipStream_t)stream,
+                       static_cast<const uint16_t*>(gate), static_cast<const uint16_t*>(up), n,
+                       static_cast<uint16_t*>(h));
+    return hipGetLastError() == hipSuccess ? NVFP4_OK : NVFP4_ERR_HIP;
 }
 
 size_t nvfp4_workspace_bytes(void) { return kWorkspaceBytes; }

@@ -52,6 +52,8 @@ def _load():
         "nvfp4_sum_f64": (I, [P, I64, P, P, SZ, P]),
         "nvfp4_scales_bytes": (I64, [I64, I64, I, I]),
         "nvfp4_quant_online": (I, [I, P, I, I64, I64, I, P, I64, I64, F, I, P, P, P, P]),
+        "nvfp4_quant_online_swiglu": (I, [I, P, P, I64, I64, P, I64, I64, F, I, P, P, P, P]),
+        "nvfp4_swiglu": (I, [P, P, I64, I64, P, P]),
         "nvfp4_channel_sq_norms_workspace_bytes": (I64, [I64, I64, I64, I64]),
         "nvfp4_channel_sq_norms": (I, [P, I, I64, I64, I64, I64, I64, I64, P, P, SZ, P]),
         "nvfp4_ldlq_workspace_bytes": (SZ, [I64, I64]),
@@ -88,6 +90,8 @@ nvfp4_sum_workspace_bytes = lib.nvfp4_sum_workspace_bytes
 nvfp4_sum_f64 = lib.nvfp4_sum_f64
 nvfp4_scales_bytes = lib.nvfp4_scales_bytes
 nvfp4_quant_online = lib.nvfp4_quant_online
+nvfp4_quant_online_swiglu = lib.nvfp4_quant_online_swiglu
+nvfp4_swiglu = lib.nvfp4_swiglu
 nvfp4_channel_sq_norms_workspace_bytes = lib.nvfp4_channel_sq_norms_workspace_bytes
 nvfp4_channel_sq_norms = lib.nvfp4_channel_sq_norms
 nvfp4_ldlq_workspace_bytes = lib.nvfp4_ldlq_workspace_bytes
@@ -380,6 +384,54 @@ def quantize_online(x: torch.Tensor, method: str, static_scale: float, block: in
         raise NVFP4Error(rc, "nvfp4_quant_online")
     if layout == "row_major" and out is None:
         sc = sc.view(rows, cols // block)
+    return q, sc
+
+
+def swiglu(gate: torch.Tensor, up: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
+    """h = bf16(silu(gate) * up) of two bfloat16 device tensors [rows, cols] (the SwiGLU
+    producer of nvfp4_quant_online_swiglu, unfused)."""
+    if not (gate.is_cuda and gate.dtype == torch.bfloat16 and up.dtype == torch.bfloat16
+            and gate.shape == up.shape and gate.dim() == 2 and gate.is_contiguous()
+            and up.is_contiguous()):
+        raise ValueError("gate and up must be contiguous bfloat16 device tensors of one 2-D shape")
+    rows, cols = gate.shape
+    h = torch.empty_like(gate) if out is None else out
+    rc = nvfp4_swiglu(_ptr(gate), _ptr(up), rows, cols, _ptr(h), _stream(gate.device))
+    if rc != 0:
+        raise NVFP4Error(rc, "nvfp4_swiglu")
+    return h
+
+
+def quantize_online_swiglu(gate: torch.Tensor, up: torch.Tensor, method: str, static_scale: float,
+                           importance: torch.Tensor | None = None, imp_groups: int = 1,
+                           imp_group_rows: int = 1, layout: str = "row_major", out=None):
+    """NVFP4 of h = bf16(silu(gate) * up) with a static global scale, h never written
+    (nvfp4_quant_online_swiglu; block 16).  Returns (q, scales) like quantize_online()."""
+    if not (gate.is_cuda and gate.dtype == torch.bfloat16 and up.dtype == torch.bfloat16
+            and gate.shape == up.shape and gate.dim() == 2 and gate.is_contiguous()
+            and up.is_contiguous()):
+        raise ValueError("gate and up must be contiguous bfloat16 device tensors of one 2-D shape")
+    rows, cols = gate.shape
+    nbytes = nvfp4_scales_bytes(rows, cols, 16, SCALE_LAYOUTS[layout])
+    if nbytes < 0:
+        raise NVFP4Error(int(nbytes), "nvfp4_scales_bytes")
+    if importance is not None and not (importance.is_cuda and importance.dtype == torch.float32
+                                       and importance.is_contiguous()
+                                       and importance.numel() == imp_groups * cols):
+        raise ValueError("importance must be a contiguous float32 device tensor [imp_groups, cols]")
+    if out is None:
+        q = torch.empty((rows, cols // 2), dtype=torch.uint8, device=gate.device)
+        sc = torch.empty(nbytes, dtype=torch.uint8, device=gate.device)
+    else:
+        q, sc = out
+    rc = nvfp4_quant_online_swiglu(METHOD_IDS[method], _ptr(gate), _ptr(up), rows, cols,
+                                   _ptr(importance), imp_groups, imp_group_rows,
+                                   ctypes.c_float(static_scale), SCALE_LAYOUTS[layout], None,
+                                   _ptr(q), _ptr(sc), _stream(gate.device))
+    if rc != 0:
+        raise NVFP4Error(rc, "nvfp4_quant_online_swiglu")
+    if layout == "row_major" and out is None:
+        sc = sc.view(rows, cols // 16)
     return q, sc
 
 

@@ -261,3 +261,26 @@ def test_ldlq_validation(nv):
     assert call(H=P(0x100004)) == -7
     assert call(wsb=wsb - 1) == -6
     assert call(ws=P(0x200010)) == -7
+
+
+@fake_pointers
+def test_swiglu_validation(nv):
+    f = nv.nvfp4_quant_online_swiglu
+
+    def call(method=2, rows=4, cols=64, up=FAKE, S=1.0, layout=0, gate=FAKE, imp=None):
+        return f(method, gate, up, rows, cols, imp, 1, 1, ctypes.c_float(S), layout, None, FAKE,
+                 FAKE, None)
+
+    assert call(up=None) == -1
+    assert call(up=P(0x100004)) == -7
+    assert call(gate=P(0x100004)) == -7
+    assert call(method=3) == -1                  # WMSE needs importance
+    assert call(S=0.0) == -5
+    assert call(cols=40) == -2
+    assert call(layout=3) == -5
+    assert call(rows=0, up=None) == 0             # empty: nothing to read
+    p = nv.nvfp4_swiglu
+    assert p(FAKE, FAKE, 4, 40, FAKE, None) == -2
+    assert p(FAKE, None, 4, 64, FAKE, None) == -1
+    assert p(FAKE, FAKE, 4, 64, P(0x100004), None) == -7
+    assert p(FAKE, FAKE, 0, 64, FAKE, None) == 0
