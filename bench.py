@@ -53,11 +53,12 @@ def parse():
                     help="also run a plain device copy of known size (for counter scaling)")
     ap.add_argument("--no-rows", action="store_true",
                     help="skip the window / reference-scale / online / GPTQ measurements")
-    ap.add_argument("--profile-config", choices=("c0", "c2", "c3", "c4"), default=None,
+    ap.add_argument("--profile-config", choices=("c0", "c2", "c3", "c4", "f3"), default=None,
                     help="run only one other configuration's launches (a few of each, for "
                          "rocprofv3 counter runs) and exit: c0 the FP32 1024x1024 matrix, c2 the "
                          "8192x8192 block-size sweep, c3 the online tensors, c4 one "
-                         "Llama-3-70B-shaped layer")
+                         "Llama-3-70B-shaped layer, f3 the fused SwiGLU quantizer and its "
+                         "unfused pair")
     ap.add_argument("--c4-layers", type=int, default=80,
                     help="Llama-3-70B-shaped layers to stream through the WMSE quantizer "
                          "(80, the default, is the whole model)")
@@ -154,6 +155,55 @@ def measure_c0(nv, workloads, torch, dev):
     return out
 
 
+def swiglu_inputs(workloads, torch, dev, tokens=8192, inter=14336):
+    """The MLP of a Llama-3-8B-shaped layer for `tokens` tokens: gate and up activations
+    [tokens, 14336] bf16 (gate ~ 3 N(0, 1), up ~ N(0, 1) with 4 outlier channels x20) and the
+    down projection's input-channel importance (one vector)."""
+    g = workloads.generator(dev, 81, 1)
+    gate = (torch.randn((tokens, inter), generator=g, device=dev) * 3.0).to(torch.bfloat16)
+    up = torch.randn((tokens, inter), generator=g, device=dev)
+    up[:, torch.randperm(inter, generator=g, device=dev)[:4]] *= 20.0
+    up = up.to(torch.bfloat16)
+    imp = workloads.column_importance(inter, g, dev, tokens=256)[None].contiguous()
+    return gate, up, imp
+
+
+def measure_fused_swiglu(nv, workloads, torch, dev):
+    """The online quantizer fused into its producer (the SwiGLU product feeding down_proj)
+    against the producer kernel followed by the online quantizer, static S, swizzled scales:
+    median of 50 single calls each (HIP events), per method, with the algorithmic HBM bytes
+    (fused: 4 B read + 0.5625 B written per element; unfused: 4 + 2 for the producer, then
+    2 + 0.5625 for the quantizer)."""
+    gate, up, imp = swiglu_inputs(workloads, torch, dev)
+    n = gate.numel()
+    h = nv.swiglu(gate, up)
+    S = 0.004
+    out = {"workload": "Llama-3-8B MLP activation of 8192 tokens: gate, up [8192, 14336] bf16 -> "
+                       "NVFP4 of bf16(silu(gate) * up), static S, swizzled scales, block 16",
+           "timing": "median of 50 single calls (HIP events)",
+           "bytes_per_element": {"fused": 4.5625, "unfused": 8.5625}}
+    ms_prod = _median_call(torch, lambda: nv.swiglu(gate, up, out=h), 50)
+    out["producer_alone_ms"] = round(ms_prod, 4)
+    for m in ("absmax", "scalesweep_mse", "scalesweep_wmse"):
+        wt = imp if m == "scalesweep_wmse" else None
+        o1 = nv.quantize_online_swiglu(gate, up, m, S, wt, layout="swizzled")
+        o2 = nv.quantize_online(h, m, S, 16, wt, layout="swizzled")
+        fused = _median_call(torch, lambda: nv.quantize_online_swiglu(gate, up, m, S, wt, layout="swizzled",
+                                                                      out=o1), 50)
+
+        def unfused():
+            nv.swiglu(gate, up, out=h)
+            nv.quantize_online(h, m, S, 16, wt, layout="swizzled", out=o2)
+
+        unf = _median_call(torch, unfused, 50)
+        out[m] = {"fused_ms": round(fused, 4), "unfused_ms": round(unf, 4),
+                  "time_saved": round(1.0 - fused / unf, 3),
+                  "fused_hbm_GBps_algorithmic": round(4.5625 * n / fused / 1e6, 1),
+                  "unfused_hbm_GBps_algorithmic": round(8.5625 * n / unf / 1e6, 1)}
+    del gate, up, h
+    return out
+
+
 def measure_rows(nv, workloads, torch, dev, layer):
     """Window variants, reference scales and the online quantizer, each on its own
     workload, as milliseconds per call and GB/s of bf16 input."""
@@ -244,6 +294,8 @@ def measure_rows(nv, workloads, torch, dev, layer):
                         "hidden8192_us_per_call": table8,
                         "importance_q_from_k_ms": round(ms_imp, 4)}
     del t
+
+    out["f3_fused_swiglu"] = measure_fused_swiglu(nv, workloads, torch, dev)
 
     # GPTQ (LDLQ) with ScaleSweep-WMSE scales fixed beforehand, q_proj and a synthetic Hessian
     g = workloads.generator(dev, 61, 99)
@@ -350,6 +402,14 @@ def profile_config(name, nv, workloads, torch, dev, copy_calibration):
             for m in ("absmax", "scalesweep_mse"):
                 run(f"c3 {nm} {list(t[nm].shape)} {m} static S swizzled",
                     lambda: nv.quantize_online(xo, m, 0.002, 16, layout="swizzled"))
+    elif name == "f3":
+        gate, up, imp = swiglu_inputs(workloads, torch, dev)
+        h = nv.swiglu(gate, up)
+        run("f3 swiglu producer [8192, 14336]", lambda: nv.swiglu(gate, up, out=h))
+        for m in ("absmax", "scalesweep_mse", "scalesweep_wmse"):
+            wt = imp if m == "scalesweep_wmse" else None
+            run(f"f3 fused {m}", lambda: nv.quantize_online_swiglu(gate, up, m, 0.004, wt, layout="swizzled"))
+            run(f"f3 unfused quantizer {m}", lambda: nv.quantize_online(h, m, 0.004, 16, wt, layout="swizzled"))
     else:
         lay = workloads.llama70b_layer(0, dev)
         xs = [lay[n][0] for n in lay]
