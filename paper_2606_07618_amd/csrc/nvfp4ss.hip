@@ -455,17 +455,17 @@ __device__ __forceinline__ void significand_group_losses_sched(const float (&y)[
 }
 
 // ---------------------------------------------------------------------------------------
-// Weighted ScaleSweep at n = 16 with provably losing candidates skipped.
+// Weighted ScaleSweep with provably losing candidates skipped.
 // ---------------------------------------------------------------------------------------
 
 // The (block, candidate) items of a wave that the in-place sweep leaves to a shared pass,
-// compacted lane by lane: owner lane in bits 5:0, candidate code in bits 12:6; each slot then
-// receives its item's loss.  A lane has at most kPrunedLow + 1 items; the slots past the last
-// possible item give the last round's idle lanes somewhere to write.  Beside the list, every
-// lane's |y| (4 x 16 bytes, stored transposed: chunk k of lane L at ay[k][L], so that the
-// stores are contiguous across the wave), read back by the lanes that score its items.
-constexpr int kPrunedLow = 7;                          // candidates d < 7 (offsets -8..-2)
-constexpr int kItemSlots = 64 * (kPrunedLow + 2);      // 8 items per lane at most, + a spare round
+// compacted block by block: the owner block's first lane in bits 5:0, candidate code in bits
+// 12:6; each slot then receives its item's loss.  A block has at most 8 items at n = 16 (64
+// blocks per wave) and 11 at n = 128 (window -11..7; 8 blocks per wave); the 64 slots past the
+// most a wave can hold give idle lanes somewhere to write.  Beside the list, every lane's |y|
+// (4 x 16 bytes, stored transposed: chunk k of lane L at ay[k][L], so that the stores are
+// contiguous across the wave), read back by the lanes that score its items.
+constexpr int kItemSlots = 64 * 8 + 64;
 struct PrunedLds {
     uint32_t item[kThreads / 64][kItemSlots];
     float4 ay[kThreads / 64][4][64];
@@ -484,19 +484,21 @@ __device__ __forceinline__ float e4m3_normal(int c) {
     return __uint_as_float(((uint32_t)c << 20) + 0x3C000000u);
 }
 
-// Losses J[d] of the WMSE window (codes cb + d, d = 0..15, offsets -8..7; all codes normal).
+// Losses J[d] of the WMSE window (codes cb + d, d = 0..NC-1, offsets -L..7 with L = NC - 8; all
+// codes normal), for blocks of n = 16 LPB elements on LPB adjacent lanes.
 //
-// Offsets -1..6 (d = 7..14) are scored in place for every block.  The other candidates are
+// Offsets -1..6 (d = L-1..L+6) are scored in place for every block.  The other candidates are
 // scored only where they can still be the window's argmin:
-//  * Lower candidates d < 7 (offsets -8..-2): their scale s is below s0 <= max|y| / 6, so the
+//  * Lower candidates d < L-1 (offsets -L..-2): their scale s is below s0 <= max|y| / 6, so the
 //    block's largest element saturates to 6 s and its term alone, w1 (y1 - 6 s)^2, bounds the
 //    candidate's loss from below.  That term is computed in the operation order the sweep uses
 //    for it (e = RN(y1 - 6 s), which the sweep's fused multiply-add also yields; then
 //    RN(RN(w1 e) e)), and a binary32 sum of non-negative terms accumulated with fused
 //    multiply-adds is never below any one of its products, so the sweep's loss of d is >= the
-//    bound.  The bound grows as s falls, so the candidates a block keeps are the top ones,
-//    d = 7 - k .. 6, and k comes from a three-step search.
-//  * Offset +7 (d = 15, code c0 + 7 >= 23): its half is offset -1, an E4M3 value of the window.
+//    bound (w1 is the weight of any one element with |y| = max|y|).  The bound grows as
+//    s falls, so the candidates a block keeps are the top ones, d = dk .. L-2, and dk comes from
+//    a binary search.
+//  * Offset +7 (d = NC-1, code c0 + 7 >= 23): its half is offset -1, an E4M3 value of the window.
 //    When 3.5 s > max|y|, every element rounds at s to a point of the half scale's grid (the
 //    Block Scale Upper Bound lemma), so its exact loss is >= that of offset -1, which wins a
 //    tie as the smaller code: +7 cannot be the argmin.  Otherwise the largest element's term,
@@ -506,46 +508,64 @@ __device__ __forceinline__ float e4m3_normal(int c) {
 // exact argmin, so skipping it (loss +inf) leaves the argmin and the band decisions exactly as
 // with the full sweep.
 //
-// The kept items of the wave (about 50 per wave on Student-t weights: mostly one round) go into
-// one list and are scored by all 64 lanes together.  A lane takes one item, reads the owner's
-// |y| from LDS (four 16-byte loads) and the owner's weights from memory (four 16-byte loads,
-// cache hits: the owner has just loaded them), all issued at once, and leaves the loss in the
-// item's slot.  The losses are the operation sequence of cand_loss, bit-identical to in-place
-// scoring.  Called in uniform control flow with all 64 lanes of the wave running; woff is the
-// element offset of this lane's weights in colw.
-template <int NC>
+// The kept (block, candidate) items of the wave (on Llama-like weights about 0.15 per block at
+// n = 16 and 2.7 at n = 128: one round, or about three) go into one list, entered by each
+// block's first lane, and are scored by all lanes together, LPB lanes per item.  Lane j of an
+// item's group reads part j of the owner block: its |y| from LDS (four 16-byte loads) and its
+// weights, at n = 16 from memory (four 16-byte loads, cache hits: the owner has just loaded
+// them), at n > 16 from the owner lane's registers (lane permutes, which keep memory latency
+// out of the several rounds); the group's partial losses are summed as in the sweep and the
+// first lane leaves the loss in the item's slot.  The losses
+// are the operation sequence of cand_loss, bit-identical to in-place scoring.  Called in uniform
+// control flow with all 64 lanes of the wave running; wblk is the offset of the block's weights
+// in colw in units of n elements, part the lane's part of its block.
+template <int NC, int LPB>
 __device__ __forceinline__ void pruned_wmse_losses(const float (&y)[kLaneElems], const float (&w)[kLaneElems],
                                                    float ymax, bool active, const Scale* tab, int cb,
                                                    float (&J)[NC], PrunedLds& lds, const float* colw,
-                                                   uint32_t woff) {
-    static_assert(NC == 16 && kPrunedLow == 7, "window offsets -8..7");
+                                                   uint32_t wblk, int part) {
+    constexpr int L = NC - 8;                        // lowest offset -L
+    constexpr int kLow = L - 1;                      // lower candidates d = 0..kLow-1
     constexpr int kTop = NC - 1;                     // d of offset +7
+    constexpr int kBits = kLow < 8 ? 3 : 4;          // binary digits of a lower count 0..kLow
+    constexpr int kG = 64 / LPB;                     // blocks (items of a round) per wave
+    static_assert(L >= 8 && kLow + 1 <= 16, "WMSE windows -8..7 / -11..7");
+    static_assert(kG * (kLow + 1) <= kItemSlots - 64, "items stay below the idle slots");
 #pragma unroll
-    for (int d = kPrunedLow; d < kPrunedLow + 8; ++d) {
-        significand_group_losses<true, 1, NC>(y, w, tab, cb, d, J, 0, kTop);
+    for (int r = 0; r < 8; ++r) {
+        significand_group_losses<true, LPB, NC>(y, w, tab, cb, r, J, kLow, kTop);
         // finished here, before the next group's quotients are formed: one group live at a time
-        asm volatile("" : "+v"(J[d]));
+#pragma unroll
+        for (int d = r; d < NC; d += 8)
+            if (d >= kLow && d < kTop) asm volatile("" : "+v"(J[d]));
     }
     asm volatile("" : "+v"(ymax));                  // the bounds below are formed after the sweep
-    float jb = J[kPrunedLow];
+    float jb = J[kLow];
 #pragma unroll
-    for (int d = kPrunedLow + 1; d < kTop; ++d) jb = fminf(jb, J[d]);   // NaN codes past 126 drop out
+    for (int d = kLow + 1; d < kTop; ++d) jb = fminf(jb, J[d]);   // NaN codes past 126 drop out
     // inactive lanes (past the last block) keep nothing
     const float thr = active ? fmaf(jb, kBand, jb) + kBandAbs : -__builtin_inff();
-    float w1 = 0.f;                                  // weight of an element with |y| = ymax
+    float w1 = 0.f;                                  // weight of an element with |y| = max|y|
 #pragma unroll
     for (int i = 0; i < kLaneElems; ++i) w1 = fabsf(y[i]) == ymax ? w[i] : w1;
+    w1 = group_max<LPB>(w1);                         // lanes without such an element offer 0
 
-    // lower candidates: d is kept iff its bound is not above thr; kept ones are d >= dk
+    // lower candidates: d is kept iff its bound is not above thr; the kept ones are d >= dk
     auto low_keep = [&](int d) {
         const float e = ymax - 6.0f * e4m3_normal(cb + d);   // 6 s is exact
         const float t = w1 * e;
         return !(t * e > thr);
     };
-    int dk = low_keep(3) ? 0 : 4;                    // first kept d is in [dk, dk + 3]
-    dk += low_keep(dk + 1) ? 0 : 2;                  // ... in [dk, dk + 1]
-    dk += low_keep(dk) ? 0 : 1;                      // ... is dk (7: none kept)
-    const uint32_t nlow = (uint32_t)(kPrunedLow - dk);
+    int dk = 0, dhi = kLow;                          // first kept d in [dk, dhi] (kLow: none)
+#pragma unroll
+    for (int it = 0; it < kBits; ++it) {
+        const int mid = (dk + dhi) >> 1;
+        if (dk < dhi) {
+            if (low_keep(mid)) dhi = mid;
+            else dk = mid + 1;
+        }
+    }
+    const uint32_t nlow = (uint32_t)(kLow - dk);
     // offset +7
     bool keep_top = false;
     {
@@ -561,47 +581,63 @@ __device__ __forceinline__ void pruned_wmse_losses(const float (&y)[kLaneElems],
         }
         keep_top = keep_top && active;
     }
-    // the lane's items: lower candidates d = 6, 5, ..., dk, then offset +7; positions in the
-    // wave's list from a prefix count over the lanes (binary digits of the counts, by ballot)
+    // each block's items (lower candidates d = kLow-1 .. dk, then offset +7), entered by its first
+    // lane; list positions from a prefix count over the blocks (binary digits, by ballot; only
+    // first lanes vote, so the count of set lanes below this lane is the count over the blocks
+    // before its block)
     const int lane = threadIdx.x & 63;
     const int wv = threadIdx.x >> 6;
+    const bool leader = part == 0;
+    auto below = [](uint64_t m) {
+        return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+    };
     uint32_t* items = lds.item[wv];
-    const uint64_t b0 = __ballot(nlow & 1u), b1 = __ballot(nlow & 2u), b2 = __ballot(nlow & 4u);
-    const uint64_t bt = __ballot(keep_top);
-    const uint32_t pos = lanes_below(b0) + 2u * lanes_below(b1) + 4u * lanes_below(b2) + lanes_below(bt);
-    const uint32_t total = (uint32_t)(__popcll(b0) + 2 * __popcll(b1) + 4 * __popcll(b2) + __popcll(bt));
+    uint32_t pos = 0u, total = 0u;
+#pragma unroll
+    for (int b = 0; b < kBits; ++b) {
+        const uint64_t m = __ballot(leader && ((nlow >> b) & 1u));
+        pos += below(m) << b;
+        total += (uint32_t)__popcll(m) << b;
+    }
+    {
+        const uint64_t m = __ballot(leader && keep_top);
+        pos += below(m);
+        total += (uint32_t)__popcll(m);
+    }
     const uint32_t idle = (uint32_t)(kItemSlots - 64 + lane);
 #pragma unroll
-    for (int j = 0; j < kPrunedLow; ++j)             // every lane stores (no branch)
-        items[(uint32_t)j < nlow ? pos + j : idle] = (uint32_t)lane | ((uint32_t)(cb + kPrunedLow - 1 - j) << 6);
-    items[keep_top ? pos + nlow : idle] = (uint32_t)lane | ((uint32_t)(cb + kTop) << 6);
+    for (int j = 0; j < kLow; ++j)                   // every lane stores (no branch)
+        items[leader && (uint32_t)j < nlow ? pos + j : idle] =
+            (uint32_t)lane | ((uint32_t)(cb + kLow - 1 - j) << 6);
+    items[leader && keep_top ? pos + nlow : idle] = (uint32_t)lane | ((uint32_t)(cb + kTop) << 6);
     if (total != 0u) {                               // uniform
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-            lds.ay[wv][k][lane] = make_float4(fabsf(y[4 * k]), fabsf(y[4 * k + 1]), fabsf(y[4 * k + 2]),
-                                              fabsf(y[4 * k + 3]));
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll 1
-        for (uint32_t r = 0; r < total; r += 64) {   // uniform; every lane takes an item or idles
-            const uint32_t pidx = r + (uint32_t)lane;
-            const uint32_t it = pidx < total ? items[pidx] : 0u;
-            const int owner = (int)(it & 63u);
-            const uint32_t ow = (uint32_t)__builtin_amdgcn_ds_bpermute(owner << 2, (int)woff);
-            const Scale sc = tab[(int)(it >> 6)];    // code 0 (no item): NaN entries, loss unused
+        const uint32_t g = (uint32_t)lane / LPB;     // this lane's item of a round, and its part
+        const int jp = lane % LPB;
+        // item of slot pidx (code 0 past the last: NaN table entries, loss unused) and where the
+        // owner block's weights for this lane's part of it start
+        auto item_at = [&](uint32_t pidx, uint32_t& it) {
+            it = pidx < total ? items[pidx] : 0u;
+            const int src = (int)(it & 63u) + jp;
+            const uint32_t ob = (uint32_t)__builtin_amdgcn_ds_bpermute(src << 2, (int)wblk);
+            return reinterpret_cast<const float4*>(colw + (uint64_t)ob * (16 * LPB) + 16 * jp);
+        };
+        // loss of the item in slot pidx, left there by the group's first lane (slots past total:
+        // idle, never read); wload(q) gives weights 4q..4q+3 of this lane's part
+        auto score = [&](uint32_t pidx, uint32_t it, auto wload) {
+            const int src = (int)(it & 63u) + jp;    // the owner block's lane for this part
+            const Scale sc = tab[(int)(it >> 6)];
             float acc0 = 0.f, acc1 = 0.f;
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {            // two halves of 8 elements: 16 operands live
+            for (int h = 0; h < 2; ++h) {            // two halves of 8 elements
                 float a[8], wo[8];
 #pragma unroll
                 for (int k = 0; k < 2; ++k) {
-                    const float4 v = lds.ay[wv][2 * h + k][owner];
+                    const float4 v = lds.ay[wv][2 * h + k][src];
                     a[4 * k] = v.x;
                     a[4 * k + 1] = v.y;
                     a[4 * k + 2] = v.z;
                     a[4 * k + 3] = v.w;
-                    const float4 q4 = reinterpret_cast<const float4*>(colw + ow + 8 * h)[k];
+                    const float4 q4 = wload(2 * h + k);
                     wo[4 * k] = q4.x;
                     wo[4 * k + 1] = q4.y;
                     wo[4 * k + 2] = q4.z;
@@ -611,23 +647,62 @@ __device__ __forceinline__ void pruned_wmse_losses(const float (&y)[kLaneElems],
                 for (int i = 0; i < 8; i += 2) {
                     const float u0 = a[i] * sc.rM, u1 = a[i + 1] * sc.rM;
                     const uint32_t pk = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(any_bits(), u0, u1, sc.cvs, 0);
-                    const float2v g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pk, sc.cvs, 0);
-                    const float e0 = fmaf(-g.x, sc.M, a[i]);
-                    const float e1 = fmaf(-g.y, sc.M, a[i + 1]);
+                    const float2v gv = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pk, sc.cvs, 0);
+                    const float e0 = fmaf(-gv.x, sc.M, a[i]);
+                    const float e1 = fmaf(-gv.y, sc.M, a[i + 1]);
                     acc0 = fmaf(wo[i] * e0, e0, acc0);
                     acc1 = fmaf(wo[i + 1] * e1, e1, acc1);
                 }
             }
-            items[pidx] = __float_as_uint(acc0 + acc1);   // slots past total: idle lanes, unread
+            const float loss = group_sum<LPB>(acc0 + acc1);
+            if (jp == 0) items[pidx] = __float_as_uint(loss);
+        };
+        auto stage_ay = [&]() {
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                lds.ay[wv][k][lane] = make_float4(fabsf(y[4 * k]), fabsf(y[4 * k + 1]), fabsf(y[4 * k + 2]),
+                                                  fabsf(y[4 * k + 3]));
+        };
+        auto wave_sync = []() {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        };
+        if constexpr (LPB == 1) {
+            // about one round per wave: the weights are loaded in the round, eight at a time
+            stage_ay();
+            wave_sync();
+#pragma unroll 1
+            for (uint32_t r = 0; r < total; r += kG) {   // uniform; every lane takes an item or idles
+                uint32_t it;
+                const float4* p4 = item_at(r + g, it);
+                score(r + g, it, [&](int q) { return p4[q]; });
+            }
+        } else {
+            // n > 16: the weights come from the owner lane's registers
+            stage_ay();
+            wave_sync();
+#pragma unroll 1
+            for (uint32_t r = 0; r < total; r += kG) {   // uniform; every group takes an item or idles
+                const uint32_t pidx = r + g;
+                const uint32_t it = pidx < total ? items[pidx] : 0u;
+                const int src = (int)(it & 63u) + jp;
+                score(pidx, it, [&](int q) {
+                    return make_float4(bperm(src, w[4 * q]), bperm(src, w[4 * q + 1]),
+                                       bperm(src, w[4 * q + 2]), bperm(src, w[4 * q + 3]));
+                });
+            }
         }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
+    // every lane of a block reads the block's losses (pos, dk, nlow, keep_top are block-wide)
+    const uint32_t bpos = LPB == 1 ? pos : (uint32_t)__shfl((int)pos, lane - part, 64);
 #pragma unroll
-    for (int d = 0; d < kPrunedLow; ++d)
-        J[d] = d >= dk ? __uint_as_float(items[pos + (uint32_t)(kPrunedLow - 1 - d)]) : __builtin_inff();
-    J[kTop] = keep_top ? __uint_as_float(items[pos + nlow]) : __builtin_inff();
+    for (int d = 0; d < kLow; ++d)
+        J[d] = d >= dk ? __uint_as_float(items[bpos + (uint32_t)(kLow - 1 - d)]) : __builtin_inff();
+    J[kTop] = keep_top ? __uint_as_float(items[bpos + nlow]) : __builtin_inff();
 }
 
 // max(|a|, |b|, c) in one instruction (abs source modifiers); c >= 0.  The inputs come from
@@ -1002,12 +1077,11 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
         row = div_bpr((uint32_t)blk_c, p);
         kb = (uint32_t)blk_c - row * p.bpr;
     }
-    uint32_t woff = 0;                // element offset of this lane's weights in colw
+    // the block's weights in colw, in units of N elements: below rows * cols / N < 2^31
+    uint32_t wblk = 0;
     if (use_w) {
-        const float* wrow = colw;
-        if (p.wgroups > 1) wrow += (int64_t)weight_group(row, p) * p.bpr * N;
-        woff = (uint32_t)((wrow - colw) + (int64_t)kb * N + part * kLaneElems);
-        load_weights(colw + woff, w);
+        wblk = (p.wgroups > 1 ? weight_group(row, p) * p.bpr : 0u) + kb;
+        load_weights(colw + (int64_t)wblk * N + part * kLaneElems, w);
     } else {
 #pragma unroll
         for (int i = 0; i < kLaneElems; ++i) w[i] = 1.0f;
@@ -1101,10 +1175,10 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
         const int c0 = floor_code(ymax, 6.0f, 1.0f / 6.0f, tab);
         const int cb = c0 - Win::L;                 // candidate d is code cb + d
         float J[NC];
-        if constexpr (WGT && N == 16) {
+        if constexpr (WGT) {
             __shared__ PrunedLds pl;
             if (__all(cb >= 8)) {
-                pruned_wmse_losses<NC>(y, w, ymax, active, tab, cb, J, pl, colw, woff);
+                pruned_wmse_losses<NC, LPB>(y, w, ymax, active, tab, cb, J, pl, colw, wblk, part);
             } else {
 #pragma unroll
                 for (int d = 0; d < NC; ++d) {
@@ -1227,7 +1301,7 @@ __global__ __launch_bounds__(kThreads) void quant_kernel(const In* __restrict__ 
                     // occupied across the sweep
                     float wx[kLaneElems];
                     if (WGT) {
-                        load_weights(colw + woff, wx);
+                        load_weights(colw + (int64_t)wblk * N + part * kLaneElems, wx);
                     } else {
 #pragma unroll
                         for (int i = 0; i < kLaneElems; ++i) wx[i] = 1.0f;

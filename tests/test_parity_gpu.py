@@ -212,8 +212,8 @@ def _lower_bound_tensor(rows, seed):
 def _lower_bound_decisions(x, w, method, block):
     """Per row (one wave of the kernels), how many (block, lower candidate) pairs the kernel
     scores and how many lower candidates the whole wave skips, from the oracle's losses and the
-    kernel's schedule: n = 16 WMSE scores offsets -1..6 and bounds the lower ones against their
-    best (offset +7 has a rule of its own, test_parity_offset_seven_rule);
+    kernel's schedule: WMSE (every n) scores offsets -1..6 and bounds the lower ones against
+    their best (offset +7 has a rule of its own, test_parity_offset_seven_rule);
     n = 16 MSE bounds offset -3 against offsets -2..7 except 5; n > 16 MSE scores -1..7, then
     the lower offsets from the highest down, each when any block of the wave may need it,
     tightening the best loss with what it scored.  The bound of a lower code c is
@@ -232,7 +232,7 @@ def _lower_bound_decisions(x, w, method, block):
             if block == 16 and not wmse:
                 scored = [c for c in range(c0 - 2, hi + 1) if c != c0 + 5]
                 lower = [c0 - 3] if c0 - 3 >= lo else []
-            elif block == 16:
+            elif wmse:
                 scored = list(range(c0 - 1, min(c0 + 6, hi) + 1))
                 lower = list(range(c0 - 2, lo - 1, -1))
             else:
@@ -240,7 +240,7 @@ def _lower_bound_decisions(x, w, method, block):
                 lower = list(range(c0 - 2, lo - 1, -1))
             i1 = int(np.argmax(y))
             info.append((min(J[c] for c in scored), lower, wb[i1] * 1.0, y[i1], J))
-        if block == 16:
+        if block == 16 or wmse:
             k = 0
             for jb, lower, w1, y1, _ in info:
                 k += sum(w1 * (y1 - 6.0 * oracle.e4m3(c)) ** 2 <= jb * (1 + 2.0 ** -14) for c in lower)
@@ -265,20 +265,23 @@ def _lower_bound_decisions(x, w, method, block):
 
 
 @pytest.mark.parametrize("method, block", [("scalesweep_mse", 16), ("scalesweep_wmse", 16),
+                                           ("scalesweep_wmse", 32), ("scalesweep_wmse", 64),
+                                           ("scalesweep_wmse", 128),
                                            ("scalesweep_mse", 32), ("scalesweep_mse", 64),
                                            ("scalesweep_mse", 128)])
 def test_parity_lower_candidate_bound(nv, method, block):
     """The sweeps skip a lower window candidate when the saturated term of the block's
-    largest element already exceeds the best loss scored so far by the re-scoring band.  WMSE
-    n = 16: rows where every block keeps all seven lower candidates (seven compaction rounds)
-    and rows where some do; MSE: waves that score a lower candidate and waves that skip it; a
-    ragged last workgroup."""
+    largest element already exceeds the best loss scored so far by the re-scoring band.  WMSE:
+    rows where every block keeps all its lower candidates (7 or 10 each: the most compaction
+    rounds a wave has) and rows where some do; MSE: waves that score a lower candidate and
+    waves that skip it; a ragged last workgroup."""
     x, w = _lower_bound_tensor(37, seed=11)
     kept, skipped = _lower_bound_decisions(x, w, method, block)   # the construction does what it says
     if method.endswith("wmse"):
-        assert all(k == 64 * 7 for k in kept[0::4]), kept
+        full = 1024 // block * (oracle.window_lower(method, block) - 1)
+        assert all(k == full for k in kept[0::4]), kept
         others = [k for r, k in enumerate(kept) if r % 4]
-        assert max(others) < 64 * 7 and sum(k > 64 for k in others) >= 3, kept
+        assert max(others) < full and sum(k > 1024 // block for k in others) >= 3, kept
     elif block == 16:
         assert sum(k > 0 for k in kept) >= 5 and sum(k == 0 for k in kept) >= 5, kept
     else:
@@ -286,48 +289,51 @@ def test_parity_lower_candidate_bound(nv, method, block):
     check(nv, method, torch.from_numpy(x).to(DEV), block, torch.from_numpy(w).to(DEV), static=1.0)
 
 
-def _offset_seven_tensor(rows, seed):
-    """[rows, 1024] binary32 for S = 1 (one 64-block row per wave), WMSE weights, built around
-    the rule for offset +7 of the n = 16 WMSE sweep.  Every block has base code c0 with mantissa
+def _offset_seven_tensor(rows, seed, block=16):
+    """[rows, 1024] binary32 for S = 1 (one row per wave), WMSE weights, built around the rule
+    for offset +7 of the WMSE sweep.  Every block of n elements has base code c0 with mantissa
     field 0, its other elements near the grid of code c0 + 7 (s7 = 15/8 s0), and its largest
     element, whose weight is small, at one of: below 3.5 s7 (the upper-bound lemma rules +7
     out), exactly 3.5 s7 (the lemma does not apply: +7 is bounded by that element's term), or
     above it (bounded; with the others on the grid of s7, +7 often wins)."""
     rng = np.random.default_rng(seed)
+    nb = 1024 // block
     x = np.zeros((rows, 1024), np.float64)
     w = rng.uniform(0.5, 2.0, 1024)
-    w[::16] = rng.uniform(0.0, 0.02, 64)                 # the largest element sits in column 0
+    w[::block] = rng.uniform(0.0, 0.02, nb)              # the largest element sits in column 0
     E = [oracle.e4m3(c) for c in range(127)]
     for r in range(rows):
-        for b in range(64):
+        for b in range(nb):
             c0 = 8 * int(rng.integers(3, 14))            # mantissa field 0
             s0, s7 = E[c0], E[c0 + 7]
             grid = np.array([0.5, 1.0, 1.5, 2.0, 3.0]) * s7
-            v = grid[rng.integers(0, 5, 16)] * (1.0 + rng.normal(0.0, 0.002 * (r % 3), 16))
+            v = grid[rng.integers(0, 5, block)] * (1.0 + rng.normal(0.0, 0.002 * (r % 3), block))
             kind = (r + b) % 3
             top = (3.5 * s7 * (1.0 - 2.0 ** -12 * rng.integers(1, 64)) if kind == 0 else
                    3.5 * s7 if kind == 1 else rng.uniform(3.5 * s7, 6.74 * s0))
             v[0] = max(top, 6.0 * s0)                    # keeps the base code at c0
             v = np.minimum(v, v[0])
-            x[r, 16 * b:16 * b + 16] = v * np.where(rng.random(16) < 0.5, -1.0, 1.0)
+            x[r, block * b:block * b + block] = v * np.where(rng.random(block) < 0.5, -1.0, 1.0)
     return x.astype(np.float32), w.astype(np.float32)
 
 
-def test_parity_offset_seven_rule(nv):
-    """WMSE n = 16: offset +7 ruled out by the upper-bound lemma, bounded at the lemma's edge,
-    and winning the window; the oracle confirms that the construction covers each case."""
-    x, w = _offset_seven_tensor(24, seed=17)
+@pytest.mark.parametrize("block, rows", [(16, 24), (32, 48), (64, 96), (128, 192)])
+def test_parity_offset_seven_rule(nv, block, rows):
+    """WMSE: offset +7 ruled out by the upper-bound lemma, bounded at the lemma's edge, and
+    winning the window; the oracle confirms that the construction covers each case."""
+    x, w = _offset_seven_tensor(rows, seed=17, block=block)
+    L = oracle.window_lower("scalesweep_wmse", block)
     ruled = edge = wins = 0
     for r in range(x.shape[0]):
-        for b in range(64):
-            y = np.abs(x[r, 16 * b:16 * b + 16])
-            res = oracle.block_sweep(y, w[16 * b:16 * b + 16], 8, 7)
+        for b in range(1024 // block):
+            y = np.abs(x[r, block * b:block * b + block])
+            res = oracle.block_sweep(y, w[block * b:block * b + block], L, 7)
             s7 = oracle.e4m3(res["c0"] + 7)
             ruled += 3.5 * s7 > y.max()
             edge += 3.5 * s7 == y.max()
             wins += res["c_win"] == res["c0"] + 7
     assert ruled > 200 and edge > 200 and wins > 20, (ruled, edge, wins)
-    check(nv, "scalesweep_wmse", torch.from_numpy(x).to(DEV), 16, torch.from_numpy(w).to(DEV),
+    check(nv, "scalesweep_wmse", torch.from_numpy(x).to(DEV), block, torch.from_numpy(w).to(DEV),
           static=1.0)
 
 
