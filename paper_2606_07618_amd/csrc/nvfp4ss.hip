@@ -462,7 +462,7 @@ __device__ __forceinline__ void significand_group_losses_sched(const float (&y)[
 // compacted block by block: the owner block's first lane in bits 5:0, candidate code in bits
 // 12:6; each slot then receives its item's loss.  A block has at most 8 items at n = 16 (64
 // blocks per wave) and 11 at n = 128 (window -11..7; 8 blocks per wave); the 64 slots past the
-// most a wave can hold give idle lanes somewhere to write.  Beside the list, every lane's |y|
+// most a wave can hold take the writes that land past the list's end.  Beside the list, every lane's |y|
 // (4 x 16 bytes, stored transposed: chunk k of lane L at ay[k][L], so that the stores are
 // contiguous across the wave), read back by the lanes that score its items.
 constexpr int kItemSlots = 64 * 8 + 64;
@@ -508,17 +508,17 @@ __device__ __forceinline__ float e4m3_normal(int c) {
 // exact argmin, so skipping it (loss +inf) leaves the argmin and the band decisions exactly as
 // with the full sweep.
 //
-// The kept (block, candidate) items of the wave (on Llama-like weights about 0.15 per block at
-// n = 16 and 2.7 at n = 128: one round, or about three) go into one list, entered by each
+// The kept (block, candidate) items of the wave (on Llama-like weights about 0.8 per block at
+// n = 16 and 4.9 at n = 128: one or two rounds, or about five) go into one list, entered by each
 // block's first lane, and are scored by all lanes together, LPB lanes per item.  Lane j of an
 // item's group reads part j of the owner block: its |y| from LDS (four 16-byte loads) and its
 // weights, at n = 16 from memory (four 16-byte loads, cache hits: the owner has just loaded
 // them), at n > 16 from the owner lane's registers (lane permutes, which keep memory latency
-// out of the several rounds); the group's partial losses are summed as in the sweep and the
-// first lane leaves the loss in the item's slot.  The losses
-// are the operation sequence of cand_loss, bit-identical to in-place scoring.  Called in uniform
-// control flow with all 64 lanes of the wave running; wblk is the offset of the block's weights
-// in colw in units of n elements, part the lane's part of its block.
+// out of the several rounds).  The group's partial losses are summed as in the sweep and the
+// first lane leaves the loss in the item's slot: the losses are the operation sequence of
+// cand_loss, bit-identical to in-place scoring.  Called in uniform control flow with all 64
+// lanes of the wave running; wblk is the offset of the block's weights in colw in units of n
+// elements, part the lane's part of its block.
 template <int NC, int LPB>
 __device__ __forceinline__ void pruned_wmse_losses(const float (&y)[kLaneElems], const float (&w)[kLaneElems],
                                                    float ymax, bool active, const Scale* tab, int cb,
@@ -530,7 +530,7 @@ __device__ __forceinline__ void pruned_wmse_losses(const float (&y)[kLaneElems],
     constexpr int kBits = kLow < 8 ? 3 : 4;          // binary digits of a lower count 0..kLow
     constexpr int kG = 64 / LPB;                     // blocks (items of a round) per wave
     static_assert(L >= 8 && kLow + 1 <= 16, "WMSE windows -8..7 / -11..7");
-    static_assert(kG * (kLow + 1) <= kItemSlots - 64, "items stay below the idle slots");
+    static_assert(kG * (kLow + 1) + kLow <= kItemSlots, "the writes past a list stay in it");
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
         significand_group_losses<true, LPB, NC>(y, w, tab, cb, r, J, kLow, kTop);
@@ -581,46 +581,45 @@ __device__ __forceinline__ void pruned_wmse_losses(const float (&y)[kLaneElems],
         }
         keep_top = keep_top && active;
     }
-    // each block's items (lower candidates d = kLow-1 .. dk, then offset +7), entered by its first
-    // lane; list positions from a prefix count over the blocks (binary digits, by ballot; only
-    // first lanes vote, so the count of set lanes below this lane is the count over the blocks
-    // before its block)
+    // each block's items are entered by its first lane; list positions from a prefix count over
+    // the blocks (binary digits, by ballot; only first lanes vote, so the count of set lanes
+    // below this lane is the count over the blocks before its block)
     const int lane = threadIdx.x & 63;
     const int wv = threadIdx.x >> 6;
     const bool leader = part == 0;
-    auto below = [](uint64_t m) {
-        return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-    };
     uint32_t* items = lds.item[wv];
     uint32_t pos = 0u, total = 0u;
 #pragma unroll
     for (int b = 0; b < kBits; ++b) {
         const uint64_t m = __ballot(leader && ((nlow >> b) & 1u));
-        pos += below(m) << b;
+        pos += lanes_below(m) << b;
         total += (uint32_t)__popcll(m) << b;
     }
     {
         const uint64_t m = __ballot(leader && keep_top);
-        pos += below(m);
+        pos += lanes_below(m);
         total += (uint32_t)__popcll(m);
     }
-    const uint32_t idle = (uint32_t)(kItemSlots - 64 + lane);
+    // A block's items: offset +7 first when kept (t = 1), then the lower candidates from d =
+    // kLow - 1 down.  Every block with items writes all kLow + 1 slots from its position, last
+    // slot first; the slots past its own items are overwritten by the blocks that follow (their
+    // writes of those slots come later, at smaller offsets), or lie past the end of the list.
+    const uint32_t t = keep_top ? 1u : 0u;
+    if (leader && nlow + t != 0u) {
+        const uint32_t v0 = (uint32_t)lane | ((uint32_t)(cb + kLow - 1) << 6);
+        uint32_t* mine = items + pos;
+        // one store per slot, in this order (a wave's LDS stores complete in issue order; the
+        // empty asm keeps the compiler from reordering or pairing them)
 #pragma unroll
-    for (int j = 0; j < kLow; ++j)                   // every lane stores (no branch)
-        items[leader && (uint32_t)j < nlow ? pos + j : idle] =
-            (uint32_t)lane | ((uint32_t)(cb + kLow - 1 - j) << 6);
-    items[leader && keep_top ? pos + nlow : idle] = (uint32_t)lane | ((uint32_t)(cb + kTop) << 6);
+        for (int j = kLow; j >= 1; --j) {
+            mine[j] = v0 + (t << 6) - ((uint32_t)j << 6);
+            asm volatile("" ::: "memory");
+        }
+        mine[0] = keep_top ? (uint32_t)lane | ((uint32_t)(cb + kTop) << 6) : v0;
+    }
     if (total != 0u) {                               // uniform
         const uint32_t g = (uint32_t)lane / LPB;     // this lane's item of a round, and its part
         const int jp = lane % LPB;
-        // item of slot pidx (code 0 past the last: NaN table entries, loss unused) and where the
-        // owner block's weights for this lane's part of it start
-        auto item_at = [&](uint32_t pidx, uint32_t& it) {
-            it = pidx < total ? items[pidx] : 0u;
-            const int src = (int)(it & 63u) + jp;
-            const uint32_t ob = (uint32_t)__builtin_amdgcn_ds_bpermute(src << 2, (int)wblk);
-            return reinterpret_cast<const float4*>(colw + (uint64_t)ob * (16 * LPB) + 16 * jp);
-        };
         // loss of the item in slot pidx, left there by the group's first lane (slots past total:
         // idle, never read); wload(q) gives weights 4q..4q+3 of this lane's part
         auto score = [&](uint32_t pidx, uint32_t it, auto wload) {
@@ -669,14 +668,17 @@ __device__ __forceinline__ void pruned_wmse_losses(const float (&y)[kLaneElems],
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         };
         if constexpr (LPB == 1) {
-            // about one round per wave: the weights are loaded in the round, eight at a time
+            // n = 16 (about one round per wave): the weights come from memory, where the owner
+            // has just loaded them
             stage_ay();
             wave_sync();
 #pragma unroll 1
             for (uint32_t r = 0; r < total; r += kG) {   // uniform; every lane takes an item or idles
-                uint32_t it;
-                const float4* p4 = item_at(r + g, it);
-                score(r + g, it, [&](int q) { return p4[q]; });
+                const uint32_t pidx = r + g;
+                const uint32_t it = pidx < total ? items[pidx] : 0u;
+                const uint32_t ob = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(it & 63u) << 2, (int)wblk);
+                const float4* p4 = reinterpret_cast<const float4*>(colw + (uint64_t)ob * 16);
+                score(pidx, it, [&](int q) { return p4[q]; });
             }
         } else {
             // n > 16: the weights come from the owner lane's registers
@@ -699,10 +701,11 @@ __device__ __forceinline__ void pruned_wmse_losses(const float (&y)[kLaneElems],
     }
     // every lane of a block reads the block's losses (pos, dk, nlow, keep_top are block-wide)
     const uint32_t bpos = LPB == 1 ? pos : (uint32_t)__shfl((int)pos, lane - part, 64);
+    const uint32_t* mine = items + bpos;
 #pragma unroll
     for (int d = 0; d < kLow; ++d)
-        J[d] = d >= dk ? __uint_as_float(items[bpos + (uint32_t)(kLow - 1 - d)]) : __builtin_inff();
-    J[kTop] = keep_top ? __uint_as_float(items[bpos + nlow]) : __builtin_inff();
+        J[d] = d >= dk ? __uint_as_float(mine[t + (uint32_t)(kLow - 1 - d)]) : __builtin_inff();
+    J[kTop] = keep_top ? __uint_as_float(mine[0]) : __builtin_inff();
 }
 
 // max(|a|, |b|, c) in one instruction (abs source modifiers); c >= 0.  The inputs come from
