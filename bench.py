@@ -38,7 +38,7 @@ VALU_PEAK_TOPS = 256 * 4 * 32 * 2.4e9 / 1e12    # 78.64 T lane-ops/s (an FMA is 
 OPS_PER_EVAL = {"scalesweep_mse": 4, "scalesweep_wmse": 5}
 CANDIDATES_16 = {"scalesweep_mse": 11, "scalesweep_wmse": 16}
 DOMINANT = "scalesweep_wmse"
-DOMINANT_SYMBOL = "quant_kernel<3, unsigned short, 16>"
+DOMINANT_SYMBOL = "quant_kernel<3, unsigned short, 16, false>"
 
 
 def parse():
@@ -53,7 +53,7 @@ def parse():
                     help="also run a plain device copy of known size (for counter scaling)")
     ap.add_argument("--no-rows", action="store_true",
                     help="skip the window / reference-scale / online / GPTQ measurements")
-    ap.add_argument("--profile-config", choices=("c0", "c2", "c3", "c4", "f3"), default=None,
+    ap.add_argument("--profile-config", choices=("c0", "c2", "c3", "c3w", "c4", "f3"), default=None,
                     help="run only one other configuration's launches (a few of each, for "
                          "rocprofv3 counter runs) and exit: c0 the FP32 1024x1024 matrix, c2 the "
                          "8192x8192 block-size sweep, c3 the online tensors, c4 one "
@@ -402,6 +402,12 @@ def profile_config(name, nv, workloads, torch, dev, copy_calibration):
             for m in ("absmax", "scalesweep_mse"):
                 run(f"c3 {nm} {list(t[nm].shape)} {m} static S swizzled",
                     lambda: nv.quantize_online(xo, m, 0.002, 16, layout="swizzled"))
+    elif name == "c3w":
+        g = workloads.generator(dev, 77)
+        xb = torch.randn((32768, 8192), generator=g, device=dev).to(torch.bfloat16)
+        for m in ("absmax", "scalesweep_mse"):
+            run(f"c3w hidden-8192 activations [32768, 8192] {m} static S swizzled",
+                lambda: nv.quantize_online(xb, m, 0.002, 16, layout="swizzled"))
     elif name == "f3":
         gate, up, imp = swiglu_inputs(workloads, torch, dev)
         h = nv.swiglu(gate, up)
