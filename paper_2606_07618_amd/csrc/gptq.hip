@@ -25,6 +25,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <utility>
+
 #include "exact_fp.h"
 #include "nvfp4ss.h"
 
@@ -94,54 +96,77 @@ __global__ __launch_bounds__(256) void init_a_kernel(const double* __restrict__ 
 }
 
 // The diagonal block [k0, k0 + 64): its D and its U, column by column from the last, in LDS.
-__global__ __launch_bounds__(kTile) void factor_diag_kernel(double* __restrict__ Uc, double* __restrict__ D,
-                                                            int64_t n, int64_t k0, int* __restrict__ status) {
+// The block's own 64 columns, right-looking: at step kk (from the last) D_kk is the updated
+// diagonal, U_i,kk = A_i,kk / D_kk for i < kk, and every A_ij (i <= j < kk) then loses
+// (U_ik U_jk) D_k, so each element receives its terms k = 63, 62, ... in the order the
+// column-by-column definition sums them.  Four threads per row, each a quarter of its
+// columns, so that a step's updates run in parallel.
+__global__ __launch_bounds__(4 * kTile) void factor_diag_kernel(double* __restrict__ Uc, double* __restrict__ D,
+                                                                int64_t n, int64_t k0, int* __restrict__ status) {
     __shared__ double Ab[kTile][kTile + 1];   // Ab[ii][jj]: A, then U, of (k0 + ii, k0 + jj)
     __shared__ double Db[kTile];
-    const int lane = threadIdx.x;
-    for (int jj = 0; jj < kTile; ++jj) Ab[lane][jj] = Uc[(k0 + jj) * n + k0 + lane];
+    const int tid = threadIdx.x;
+    for (int t = tid; t < kTile * kTile; t += 4 * kTile) {
+        const int jj = t / kTile, ii = t % kTile;                 // coalesced over ii
+        Ab[ii][jj] = Uc[(k0 + jj) * n + k0 + ii];
+    }
     __syncthreads();
-    for (int jj = kTile - 1; jj >= 0; --jj) {
-        if (lane == 0) {
-            double d = Ab[jj][jj];
-            for (int kk = kTile - 1; kk > jj; --kk) {
-                const double u = Ab[jj][kk];
-                d = d - (u * u) * Db[kk];
-            }
-            Db[jj] = d;
-        }
-        double acc = Ab[lane][jj];
-        for (int kk = kTile - 1; kk > jj; --kk) acc = acc - (Ab[lane][kk] * Ab[jj][kk]) * Db[kk];
+    const int i = tid >> 2, q = tid & 3;
+    for (int kk = kTile - 1; kk >= 0; --kk) {
+        const double d = Ab[kk][kk];
+        if (q == 0 && i < kk) Ab[i][kk] = Ab[i][kk] / d;           // U_i,kk
+        if (tid == 0) Db[kk] = d;
         __syncthreads();
-        if (lane < jj) Ab[lane][jj] = acc / Db[jj];
+        if (i < kk) {
+            const double ui = Ab[i][kk];
+            for (int j = i + q; j < kk; j += 4) Ab[i][j] = Ab[i][j] - (ui * Ab[j][kk]) * d;
+        }
         __syncthreads();
     }
-    for (int jj = lane + 1; jj < kTile; ++jj) Uc[(k0 + jj) * n + k0 + lane] = Ab[lane][jj];
-    const double d = Db[lane];
-    D[k0 + lane] = d;
-    if (!(d > 0.0) || !isfinite(d)) status[0] = 1;               // not positive definite
+    for (int t = tid; t < kTile * kTile; t += 4 * kTile) {
+        const int jj = t / kTile, ii = t % kTile;
+        if (ii < jj) Uc[(k0 + jj) * n + k0 + ii] = Ab[ii][jj];
+    }
+    if (tid < kTile) {
+        const double d = Db[tid];
+        D[k0 + tid] = d;
+        if (!(d > 0.0) || !isfinite(d)) status[0] = 1;           // not positive definite
+    }
 }
 
-// Rows above the block (i < k0), 64 per workgroup: U_ij for the block's columns, each row a
-// triangular solve from the block's last column, with the row's new values kept in LDS.
-__global__ __launch_bounds__(kTile) void factor_panel_kernel(double* __restrict__ Uc,
-                                                             const double* __restrict__ D, int64_t n,
-                                                             int64_t k0) {
+// Rows above the block (i < k0), 64 per workgroup, four threads per row: U_ij for the block's
+// columns, each row a triangular solve from the block's last column, right-looking: at step
+// kk the row's value of column kk is final, U_i,kk = A_i,kk / D_kk, and each of the row's
+// columns j < kk loses (U_i,kk U_j,kk) D_kk, the threads of the row taking every fourth
+// column.  So each value receives its terms kk = 63, 62, ... in the order the column-by-column
+// definition sums them.  The rows' starting values are loaded together first.
+__global__ __launch_bounds__(4 * kTile) void factor_panel_kernel(double* __restrict__ Uc,
+                                                                 const double* __restrict__ D, int64_t n,
+                                                                 int64_t k0) {
     __shared__ double Ub[kTile][kTile + 1];   // Ub[jj][kk] = U_{k0+jj, k0+kk}, jj < kk
-    __shared__ double ui[kTile][kTile];       // ui[kk][lane] = U_{i, k0+kk}
+    __shared__ double ui[kTile][kTile + 1];   // ui[rr][kk]: A, then U, of (i0 + rr, k0 + kk)
     __shared__ double Db[kTile];
-    const int lane = threadIdx.x;
-    for (int kk = 0; kk < kTile; ++kk) Ub[lane][kk] = Uc[(k0 + kk) * n + k0 + lane];
-    Db[lane] = D[k0 + lane];
+    const int tid = threadIdx.x;
+    const int64_t i0 = (int64_t)blockIdx.x * kTile;
+    for (int t = tid; t < kTile * kTile; t += 4 * kTile) {
+        const int kk = t / kTile, m = t % kTile;                  // coalesced over m
+        Ub[m][kk] = Uc[(k0 + kk) * n + k0 + m];
+        if (i0 + m < k0) ui[m][kk] = Uc[(k0 + kk) * n + i0 + m];
+    }
+    if (tid < kTile) Db[tid] = D[k0 + tid];
     __syncthreads();
-    const int64_t i = (int64_t)blockIdx.x * kTile + lane;
-    if (i >= k0) return;
-    for (int jj = kTile - 1; jj >= 0; --jj) {
-        double acc = Uc[(k0 + jj) * n + i];
-        for (int kk = kTile - 1; kk > jj; --kk) acc = acc - (ui[kk][lane] * Ub[jj][kk]) * Db[kk];
-        const double u = acc / Db[jj];
-        ui[jj][lane] = u;
-        Uc[(k0 + jj) * n + i] = u;
+    const int rr = tid >> 2, q = tid & 3;
+    const int64_t i = i0 + rr;
+    if (i >= k0) return;                     // whole quads; rows share nothing
+    for (int kk = kTile - 1; kk >= 0; --kk) {
+        const double dk = Db[kk];
+        const double u = ui[rr][kk] / dk;    // the four threads alike
+        if (q == 0) Uc[(k0 + kk) * n + i] = u;
+        for (int j = q; j < kk; j += 4) ui[rr][j] = ui[rr][j] - (u * Ub[j][kk]) * dk;
+        // the row's next column (updated by one of its threads) is read by all four next
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
 }
 
@@ -201,49 +226,86 @@ __global__ __launch_bounds__(256) void init_x_kernel(const In* __restrict__ w, c
     X[t] = (double)load_w<In>(w, r * n + perm[a]);
 }
 
-// One lane per row (64 rows per workgroup), walking the tile in order: value a of the tile is
-// its running value from X plus the products of the tile's earlier errors (kept in LDS, one
-// column per lane) with U, added from b = a0 up; then it is quantized and its error stored.
+// f(integral_constant<int, B>) for B = 0, 1, ... in order (the calls unrolled at compile time).
+template <typename F, int... B>
+__device__ __forceinline__ void for_each_index(F&& f, std::integer_sequence<int, B...>) {
+    (f(std::integral_constant<int, B>()), ...);
+}
+
+// Lane l of a quad broadcasts v to the quad's four lanes (a DPP quad permutation).
+template <int L>
+__device__ __forceinline__ double quad_bcast(double v) {
+    constexpr int ctrl = L * 0x55;                    // quad_perm(L, L, L, L)
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, ctrl, 0xF, 0xF, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), ctrl, 0xF, 0xF, false);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// One tile of 64 columns, right-looking, four lanes (a quad) per row and 64 rows per
+// workgroup: lane p of a quad holds the running values of tile columns 16p .. 16p + 15 in
+// registers.  Column b's value is broadcast to the quad, which quantizes it (every lane the
+// same operations, so the same error), and each lane then adds error_b * U_b,a to each of its
+// columns a > b.  Every value thus receives its terms b = a0, a0 + 1, ... in ascending order,
+// as the sequential definition adds them.  The row's weights and scale bytes are staged in LDS
+// (read by the four lanes alike), U's tile block too.
 template <typename In>
-__global__ __launch_bounds__(kTile) void tile_kernel(const In* __restrict__ w, const int* __restrict__ perm,
-                                                     const double* __restrict__ Uc,
-                                                     const uint8_t* __restrict__ scales,
-                                                     const float* __restrict__ tensor_scale,
-                                                     int64_t rows, int64_t n, int block, int64_t a0,
-                                                     const double* __restrict__ X,
-                                                     double* __restrict__ Et,
-                                                     uint8_t* __restrict__ codes) {
+__global__ __launch_bounds__(4 * kTile) void tile_kernel(const In* __restrict__ w, const int* __restrict__ perm,
+                                                         const double* __restrict__ Uc,
+                                                         const uint8_t* __restrict__ scales,
+                                                         const float* __restrict__ tensor_scale,
+                                                         int64_t rows, int64_t n, int block, int64_t a0,
+                                                         const double* __restrict__ X,
+                                                         double* __restrict__ Et,
+                                                         uint8_t* __restrict__ codes) {
     __shared__ double T[kTile][kTile];      // T[b][a] = U_{a0+b, a0+a}
-    __shared__ double es[kTile][kTile];     // es[b][lane]: error of tile column b, this lane's row
+    __shared__ float wsv[kTile][kTile + 1]; // wsv[rr][a]: the weight of tile column a, row rr
+    __shared__ uint8_t scs[kTile][kTile];   // scs[rr][a]: its block's scale code
     __shared__ int pc[kTile];
-    const int lane = threadIdx.x;
-#pragma unroll 8
-    for (int a = 0; a < kTile; ++a) T[lane][a] = Uc[(a0 + a) * n + a0 + lane];   // coalesced
-    pc[lane] = perm[a0 + lane];
+    const int tid = threadIdx.x;
+    for (int t = tid; t < kTile * kTile; t += 4 * kTile) {
+        const int a = t / kTile, b = t % kTile;                   // coalesced over b
+        T[b][a] = Uc[(a0 + a) * n + a0 + b];
+    }
+    if (tid < kTile) pc[tid] = perm[a0 + tid];
     __syncthreads();
-    const int64_t r = (int64_t)blockIdx.x * kTile + lane;
-    if (r >= rows) return;
+    const int rr = tid >> 2, p = tid & 3;
+    const int64_t r = (int64_t)blockIdx.x * kTile + rr;
+    if (r >= rows) return;                   // whole quads: the broadcasts stay inside live rows
+    const int64_t nb = n / block;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {           // this lane's share of the row's weights and scales
+        const int a = 16 * p + j, c = pc[a];
+        wsv[rr][a] = load_w<In>(w, r * n + c);
+        scs[rr][a] = scales[r * nb + c / block];
+    }
+    double x[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) x[j] = X[r * n + a0 + 16 * p + j];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");   // the quad's LDS stores, then reads
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     const float S = tensor_scale[0];
     const double Sd = (double)S;
-    const int64_t nb = n / block;
-#pragma unroll 1
-    for (int a = 0; a < kTile; ++a) {
-        double x = X[r * n + a0 + a];
-#pragma unroll 4
-        for (int b = 0; b < a; ++b) x = x + es[b][lane] * T[b][a];
-        const int c = pc[a];
-        const double wv = (double)load_w<In>(w, r * n + c);
-        const float y = __fdiv_rn(__double2float_rn(x), S);
-        const double s = e4m3_f64(scales[r * nb + c / block]);
+    auto column = [&](auto bc) {
+        constexpr int b = decltype(bc)::value, pb = b / 16, jb = b % 16;
+        const double xb = quad_bcast<pb>(x[jb]);
+        const float y = __fdiv_rn(__double2float_rn(xb), S);
+        const double s = e4m3_f64(scs[rr][b]);
         const int k = round_fp4_index(fabs((double)y), s);
         double wq = e2m1_value(k) * s * Sd;
         const bool neg = signbit(y);
         if (neg) wq = -wq;
-        const double e = wv - wq;
-        codes[r * n + c] = (uint8_t)((neg ? 8 : 0) | k);
-        es[a][lane] = e;
-        Et[r * kTile + a] = e;
-    }
+        const double e = (double)wsv[rr][b] - wq;
+        if (p == pb) {
+            codes[r * n + pc[b]] = (uint8_t)((neg ? 8 : 0) | k);
+            Et[r * kTile + b] = e;
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+            if (16 * p + j > b) x[j] = x[j] + e * T[b][16 * p + j];
+    };
+    for_each_index(column, std::make_integer_sequence<int, kTile>());
 }
 
 // X[r][k] += sum over the tile's b (in order) of Et[r][b] * U_{a0+b, k}, for k >= a0 + 64:
@@ -348,9 +410,9 @@ int run_ldlq(const void* wv, int64_t rows, int64_t n, int block, const double* H
     hipLaunchKernelGGL(init_a_kernel, dim3(blocks_for(n * n, 256)), dim3(256), 0, st, H, perm, lambda,
                        n, Uc);
     for (int64_t k0 = n - kTile; k0 >= 0; k0 -= kTile) {
-        hipLaunchKernelGGL(factor_diag_kernel, dim3(1), dim3(kTile), 0, st, Uc, D, n, k0, status);
+        hipLaunchKernelGGL(factor_diag_kernel, dim3(1), dim3(4 * kTile), 0, st, Uc, D, n, k0, status);
         if (k0 > 0) {
-            hipLaunchKernelGGL(factor_panel_kernel, dim3(blocks_for(k0, kTile)), dim3(kTile), 0, st, Uc,
+            hipLaunchKernelGGL(factor_panel_kernel, dim3(blocks_for(k0, kTile)), dim3(4 * kTile), 0, st, Uc,
                                D, n, k0);
             const unsigned tiles = (unsigned)(k0 / kTile);
             hipLaunchKernelGGL(factor_trailing_kernel, dim3(tiles, tiles), dim3(256), 0, st, Uc, D, n, k0);
@@ -360,7 +422,7 @@ int run_ldlq(const void* wv, int64_t rows, int64_t n, int block, const double* H
     hipLaunchKernelGGL(init_x_kernel<In>, dim3(blocks_for(rows * n, 256)), dim3(256), 0, st, w, perm,
                        rows, n, X);
     for (int64_t a0 = 0; a0 < n; a0 += kTile) {
-        hipLaunchKernelGGL(tile_kernel<In>, dim3(blocks_for(rows, kTile)), dim3(kTile), 0, st, w, perm, Uc,
+        hipLaunchKernelGGL(tile_kernel<In>, dim3(blocks_for(rows, kTile)), dim3(4 * kTile), 0, st, w, perm, Uc,
                            scales, S, rows, n, block, a0, X, Et, codes);
         const int64_t rest = n - a0 - kTile;
         if (rest > 0)
