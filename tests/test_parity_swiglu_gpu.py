@@ -39,6 +39,26 @@ def mlp_inputs(rows, cols, seed, extremes=False):
     return gate.to(torch.bfloat16).contiguous(), up.to(torch.bfloat16).contiguous()
 
 
+def test_swiglu_every_bfloat16_gate(nv):
+    """Every finite bfloat16 gate pattern (65,280 of them, padded to [4096, 16]), once with up = 1
+    and once with up drawn from N(0, 1) with outliers: the producer's tabulated silu and its
+    closed forms outside the table (|g| < 2^-40 and |g| >= 128) against the oracle, bit for bit."""
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    finite = np.isfinite(oracle.bf16_to_f32(bits))
+    gb = bits[finite]
+    gb = np.concatenate([gb, np.zeros(4096 * 16 - gb.size, np.uint16)]).reshape(4096, 16)
+    gate = torch.from_numpy(gb.view(np.int16)).to(DEV).view(torch.bfloat16)
+    g = workloads.generator(DEV, 81, 7)
+    for up in (torch.ones((4096, 16), device=DEV),
+               torch.randn((4096, 16), generator=g, device=DEV) * 3.0):
+        up = up.to(torch.bfloat16).contiguous()
+        h = nv.swiglu(gate, up)
+        torch.cuda.synchronize()
+        want = oracle.swiglu(workloads.bf16_bits(gate), workloads.bf16_bits(up))
+        got = workloads.bf16_bits(h)
+        assert np.array_equal(got, want), describe_mismatch(got, want, "h")
+
+
 @pytest.mark.parametrize("shape", [(67, 512), (3, 1024), (130, 64)])
 def test_swiglu_producer_matches_oracle(nv, shape):
     gate, up = mlp_inputs(*shape, seed=shape[0], extremes=True)
