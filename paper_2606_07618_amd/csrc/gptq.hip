@@ -6,18 +6,19 @@
 // with Hp = (U + I) D (U + I)^T the factorization of the damped, reordered Hessian (U strictly
 // upper triangular).  LDLQ and GPTQ give the same result.  Everything is binary64 with a
 // fixed order of correctly rounded operations per value:
-//   * factor: Hp is factored in place (column-major) in 64-column blocks from the last:
-//     the block's own columns in LDS, one column at a time from its last; then the rows
-//     above it, each a 64-column triangular solve; then the block's contribution
-//     (U_ik U_jk) D_k, k walked downwards, is subtracted from the rest of the upper triangle
-//     in 64 x 64 tiles.  So each element receives its terms k = n-1, ..., j+1 in that order.
-//   * quantize: columns are taken in tiles of 64.  A tile kernel gives each row one lane that
-//     walks the tile in order: x_a is its running value plus the products of the tile's
-//     earlier errors (LDS) with U (staged in LDS), added in order; then x_a is quantized and
-//     its error kept.  A trailing-update kernel then adds the tile's 64 errors times U to every
-//     later column, term by term in tile order, in 64 x 64 output blocks with 4 x 4 values
-//     per lane.  Every x_a therefore receives its terms b = 0, 1, ... in ascending order, as
-//     the sequential definition adds them.
+//   * factor: Hp is factored in place (column-major) in 64-column blocks from the last: the
+//     block's own columns in LDS, right-looking from its last column (each column's updates
+//     to the block's remaining triangle in parallel); then the rows above it, each a 64-column
+//     triangular solve, also right-looking; then the block's contribution (U_ik U_jk) D_k, k
+//     walked downwards, is subtracted from the rest of the upper triangle in 64 x 64 tiles.
+//     So each element receives its terms k = n-1, ..., j+1 in that order.
+//   * quantize: columns are taken in tiles of 64.  A tile kernel gives each row a quad of
+//     lanes holding the tile's running values in registers: column b's value is quantized and
+//     its error times U added to the tile's later columns, b = a0, a0 + 1, ... in order.  A
+//     trailing-update kernel then adds the tile's 64 errors times U to every later column,
+//     term by term in tile order, in 64 x 64 output blocks with 4 x 4 values per lane.  Every
+//     x_a therefore receives its terms b = 0, 1, ... in ascending order, as the sequential
+//     definition adds them.
 // Q(x) is the quantizers' rounding: y = RN32(RN32(x) / S), nibble sign(y) << 3 | RNE_FP4(|y| /
 // s), w^ = +-E2M1 * s * S (exact in binary64).
 #include <hip/hip_runtime.h>
