@@ -134,3 +134,26 @@ def test_online_full_size_attention_and_activations(nv):
         run_online(nv, x, "scalesweep_wmse", S, imp[name], groups, T if name != "act" else 1,
                    "swizzled", rows=rows)
         run_online(nv, x, "scalesweep_mse", S, None, 1, 1, "swizzled", rows=rows)
+
+
+def test_online_importance_offsets_past_2_32(nv):
+    """Per-row importance vectors (imp_groups = rows) over more than 2^32 weights: the kernels
+    address a block's weights in units of the block size, so rows whose weights start past
+    2^32 elements read their own vectors.  [133120, 32768] bf16 (4.36 G elements, 8.7 GB) with a
+    [133120, 32768] binary32 importance array (17.4 GB), WMSE with static S, row-major scales;
+    sampled rows on both sides of the 2^32 mark against the oracle."""
+    rows, cols = (1 << 17) + 2048, 1 << 15
+    g = workloads.generator(DEV, 91, 1)
+    x = torch.randn((rows, cols), generator=g, device=DEV, dtype=torch.bfloat16)
+    imp = torch.rand((rows, cols), generator=g, device=DEV, dtype=torch.float32) + 0.1
+    q, sc = nv.quantize_online(x, "scalesweep_wmse", 0.004, 16, imp, rows, 1)
+    torch.cuda.synchronize()
+    edge = (1 << 32) // cols                                       # first row past 2^32
+    for r in (0, 12345, edge - 1, edge, edge + 1, rows - 1):
+        xr = workloads.host_array(x[r:r + 1])
+        ir = imp[r:r + 1].cpu().numpy()
+        q_ref, sc_ref = oracle.quantize_online("scalesweep_wmse", xr, 0.004, 16, ir)
+        assert np.array_equal(q[r].cpu().numpy(), q_ref[0]), r
+        assert np.array_equal(sc[r].cpu().numpy(), sc_ref.reshape(-1)), r
+    del x, imp, q, sc
+    torch.cuda.empty_cache()
