@@ -173,39 +173,45 @@ __global__ __launch_bounds__(4 * kTile) void factor_panel_kernel(double* __restr
 
 // A_ij -= sum over the block's k, downwards, of (U_ik U_jk) D_k for i <= j < k0: one 64 x 64
 // tile of the upper triangle per workgroup (tiles below it exit), 4 x 4 values per lane.
-__global__ __launch_bounds__(256) void factor_trailing_kernel(double* __restrict__ Uc,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void factor_trailing_kernel(double* __restrict__ Uc,
                                                               const double* __restrict__ D,
                                                               int64_t n, int64_t k0) {
     const int64_t bi = blockIdx.y, bj = blockIdx.x;
     if (bi > bj) return;
-    __shared__ double Ui[kTile][kTile + 1];   // Ui[ii][kk] = U_{i0+ii, k0+kk}
-    __shared__ double Uj[kTile][kTile + 1];
+    // the block's 64 k in two halves of 32 (the upper first), so that four workgroups fit a
+    // CU's LDS: four waves per SIMD to issue the binary64 chains
+    constexpr int kHalf = kTile / 2;
+    __shared__ double Ui[kTile][kHalf + 1];   // Ui[ii][kk] = U_{i0+ii, k0+h+kk}
+    __shared__ double Uj[kTile][kHalf + 1];
     __shared__ double Dk[kTile];
     const int64_t i0 = bi * kTile, j0 = bj * kTile;
-    for (int t = threadIdx.x; t < kTile * kTile; t += 256) {
-        const int kk = t / kTile, r = t % kTile;                  // coalesced over r
-        Ui[r][kk] = Uc[(k0 + kk) * n + i0 + r];
-        Uj[r][kk] = Uc[(k0 + kk) * n + j0 + r];
-    }
     if (threadIdx.x < kTile) Dk[threadIdx.x] = D[k0 + threadIdx.x];
-    __syncthreads();
     const int tr = threadIdx.x / 16, tc = threadIdx.x % 16;
     double acc[4][4];
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
         for (int b = 0; b < 4; ++b) acc[a][b] = Uc[(j0 + tc + 16 * b) * n + i0 + tr + 16 * a];
-    for (int kk = kTile - 1; kk >= 0; --kk) {
-        double ua[4], ub[4];
+    for (int h = kHalf; h >= 0; h -= kHalf) {
+        __syncthreads();                                          // the previous half is used
+        for (int t = threadIdx.x; t < kTile * kHalf; t += 256) {
+            const int kk = t / kTile, r = t % kTile;              // coalesced over r
+            Ui[r][kk] = Uc[(k0 + h + kk) * n + i0 + r];
+            Uj[r][kk] = Uc[(k0 + h + kk) * n + j0 + r];
+        }
+        __syncthreads();
+        for (int kk = kHalf - 1; kk >= 0; --kk) {
+            double ua[4], ub[4];
 #pragma unroll
-        for (int a = 0; a < 4; ++a) ua[a] = Ui[tr + 16 * a][kk];
+            for (int a = 0; a < 4; ++a) ua[a] = Ui[tr + 16 * a][kk];
 #pragma unroll
-        for (int b = 0; b < 4; ++b) ub[b] = Uj[tc + 16 * b][kk];
-        const double dk = Dk[kk];
+            for (int b = 0; b < 4; ++b) ub[b] = Uj[tc + 16 * b][kk];
+            const double dk = Dk[h + kk];
 #pragma unroll
-        for (int a = 0; a < 4; ++a)
+            for (int a = 0; a < 4; ++a)
 #pragma unroll
-            for (int b = 0; b < 4; ++b) acc[a][b] = acc[a][b] - (ua[a] * ub[b]) * dk;
+                for (int b = 0; b < 4; ++b) acc[a][b] = acc[a][b] - (ua[a] * ub[b]) * dk;
+        }
     }
 #pragma unroll
     for (int a = 0; a < 4; ++a)
@@ -310,22 +316,17 @@ __global__ __launch_bounds__(4 * kTile) void tile_kernel(const In* __restrict__ 
 }
 
 // X[r][k] += sum over the tile's b (in order) of Et[r][b] * U_{a0+b, k}, for k >= a0 + 64:
-// one 64 x 64 output block per workgroup, 4 x 4 values per lane.
-__global__ __launch_bounds__(256) void trailing_kernel(const double* __restrict__ Et,
+// one 64 x 64 output block per workgroup, 4 x 4 values per lane, the terms staged 32 at a time
+// (so that four workgroups fit a CU's LDS: four waves per SIMD to issue the binary64 chains).
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void trailing_kernel(const double* __restrict__ Et,
                                                        const double* __restrict__ Uc,
                                                        int64_t rows, int64_t n, int64_t a0,
                                                        double* __restrict__ X) {
-    __shared__ double Es[kTile][kTile + 1];    // Es[row][b]
-    __shared__ double Us[kTile][kTile + 1];    // Us[b][col]
+    constexpr int kHalf = kTile / 2;
+    __shared__ double Es[kTile][kHalf + 1];    // Es[row][b]
+    __shared__ double Us[kHalf][kTile + 1];    // Us[b][col]
     const int64_t r0 = (int64_t)blockIdx.y * kTile;
     const int64_t k0 = a0 + kTile + (int64_t)blockIdx.x * kTile;
-    for (int t = threadIdx.x; t < kTile * kTile; t += 256) {
-        const int rr = t / kTile, b = t % kTile;
-        Es[rr][b] = r0 + rr < rows ? Et[(r0 + rr) * kTile + b] : 0.0;
-        const int cc = t / kTile, bb = t % kTile;                 // coalesced over b
-        Us[bb][cc] = k0 + cc < n ? Uc[(k0 + cc) * n + a0 + bb] : 0.0;
-    }
-    __syncthreads();
     const int tr = threadIdx.x / 16, tc = threadIdx.x % 16;      // 16 x 16 lanes, 4 x 4 each
     double acc[4][4];
 #pragma unroll
@@ -335,16 +336,26 @@ __global__ __launch_bounds__(256) void trailing_kernel(const double* __restrict_
             const int64_t r = r0 + tr + 16 * i, k = k0 + tc + 16 * j;
             acc[i][j] = (r < rows && k < n) ? X[r * n + k] : 0.0;
         }
-    for (int b = 0; b < kTile; ++b) {
-        double e[4], u[4];
+    for (int h = 0; h < kTile; h += kHalf) {
+        __syncthreads();                                          // the previous half is used
+        for (int t = threadIdx.x; t < kTile * kHalf; t += 256) {
+            const int rr = t / kHalf, b = t % kHalf;              // coalesced over b
+            Es[rr][b] = r0 + rr < rows ? Et[(r0 + rr) * kTile + h + b] : 0.0;
+            const int cc = t / kHalf, bb = t % kHalf;
+            Us[bb][cc] = k0 + cc < n ? Uc[(k0 + cc) * n + a0 + h + bb] : 0.0;
+        }
+        __syncthreads();
+        for (int b = 0; b < kHalf; ++b) {
+            double e[4], u[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) e[i] = Es[tr + 16 * i][b];
+            for (int i = 0; i < 4; ++i) e[i] = Es[tr + 16 * i][b];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) u[j] = Us[b][tc + 16 * j];
+            for (int j = 0; j < 4; ++j) u[j] = Us[b][tc + 16 * j];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = acc[i][j] + e[i] * u[j];
+                for (int j = 0; j < 4; ++j) acc[i][j] = acc[i][j] + e[i] * u[j];
+        }
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
