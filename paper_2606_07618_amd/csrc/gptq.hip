@@ -102,37 +102,47 @@ __global__ __launch_bounds__(256) void init_a_kernel(const double* __restrict__ 
 // (U_ik U_jk) D_k, so each element receives its terms k = 63, 62, ... in the order the
 // column-by-column definition sums them.  Four threads per row, each a quarter of its
 // columns, so that a step's updates run in parallel.
-__global__ __launch_bounds__(4 * kTile) void factor_diag_kernel(double* __restrict__ Uc, double* __restrict__ D,
-                                                                int64_t n, int64_t k0, int* __restrict__ status) {
-    __shared__ double Ab[kTile][kTile + 1];   // Ab[ii][jj]: A, then U, of (k0 + ii, k0 + jj)
-    __shared__ double Db[kTile];
+struct DiagLds {
+    double Ab[kTile][kTile + 1];   // Ab[ii][jj]: A, then U, of (k0 + ii, k0 + jj)
+    double Db[kTile];
+};
+
+__device__ __forceinline__ void factor_diag_body(double* __restrict__ Uc, double* __restrict__ D,
+                                                 int64_t n, int64_t k0, int* __restrict__ status,
+                                                 DiagLds& L) {
     const int tid = threadIdx.x;
     for (int t = tid; t < kTile * kTile; t += 4 * kTile) {
         const int jj = t / kTile, ii = t % kTile;                 // coalesced over ii
-        Ab[ii][jj] = Uc[(k0 + jj) * n + k0 + ii];
+        L.Ab[ii][jj] = Uc[(k0 + jj) * n + k0 + ii];
     }
     __syncthreads();
     const int i = tid >> 2, q = tid & 3;
     for (int kk = kTile - 1; kk >= 0; --kk) {
-        const double d = Ab[kk][kk];
-        if (q == 0 && i < kk) Ab[i][kk] = Ab[i][kk] / d;           // U_i,kk
-        if (tid == 0) Db[kk] = d;
+        const double d = L.Ab[kk][kk];
+        if (q == 0 && i < kk) L.Ab[i][kk] = L.Ab[i][kk] / d;       // U_i,kk
+        if (tid == 0) L.Db[kk] = d;
         __syncthreads();
         if (i < kk) {
-            const double ui = Ab[i][kk];
-            for (int j = i + q; j < kk; j += 4) Ab[i][j] = Ab[i][j] - (ui * Ab[j][kk]) * d;
+            const double ui = L.Ab[i][kk];
+            for (int j = i + q; j < kk; j += 4) L.Ab[i][j] = L.Ab[i][j] - (ui * L.Ab[j][kk]) * d;
         }
         __syncthreads();
     }
     for (int t = tid; t < kTile * kTile; t += 4 * kTile) {
         const int jj = t / kTile, ii = t % kTile;
-        if (ii < jj) Uc[(k0 + jj) * n + k0 + ii] = Ab[ii][jj];
+        if (ii < jj) Uc[(k0 + jj) * n + k0 + ii] = L.Ab[ii][jj];
     }
     if (tid < kTile) {
-        const double d = Db[tid];
+        const double d = L.Db[tid];
         D[k0 + tid] = d;
         if (!(d > 0.0) || !isfinite(d)) status[0] = 1;           // not positive definite
     }
+}
+
+__global__ __launch_bounds__(4 * kTile) void factor_diag_kernel(double* __restrict__ Uc, double* __restrict__ D,
+                                                                int64_t n, int64_t k0, int* __restrict__ status) {
+    __shared__ DiagLds L;
+    factor_diag_body(Uc, D, n, k0, status, L);
 }
 
 // Rows above the block (i < k0), 64 per workgroup, four threads per row: U_ij for the block's
@@ -172,20 +182,22 @@ __global__ __launch_bounds__(4 * kTile) void factor_panel_kernel(double* __restr
 }
 
 // A_ij -= sum over the block's k, downwards, of (U_ik U_jk) D_k for i <= j < k0: one 64 x 64
-// tile of the upper triangle per workgroup (tiles below it exit), 4 x 4 values per lane.
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void factor_trailing_kernel(double* __restrict__ Uc,
-                                                              const double* __restrict__ D,
-                                                              int64_t n, int64_t k0) {
-    const int64_t bi = blockIdx.y, bj = blockIdx.x;
+// tile (bi, bj) of the upper triangle per workgroup (tiles below it exit), 4 x 4 values per
+// lane; the block's 64 k in two halves of 32 (the upper first), so that four workgroups fit a
+// CU's LDS: four waves per SIMD to issue the binary64 chains.
+constexpr int kHalf = kTile / 2;
+struct FTrailLds {
+    double Ui[kTile][kHalf + 1];   // Ui[ii][kk] = U_{i0+ii, k0+h+kk}
+    double Uj[kTile][kHalf + 1];
+    double Dk[kTile];
+};
+
+__device__ __forceinline__ void factor_trailing_body(double* __restrict__ Uc, const double* __restrict__ D,
+                                                     int64_t n, int64_t k0, int64_t bi, int64_t bj,
+                                                     FTrailLds& L) {
     if (bi > bj) return;
-    // the block's 64 k in two halves of 32 (the upper first), so that four workgroups fit a
-    // CU's LDS: four waves per SIMD to issue the binary64 chains
-    constexpr int kHalf = kTile / 2;
-    __shared__ double Ui[kTile][kHalf + 1];   // Ui[ii][kk] = U_{i0+ii, k0+h+kk}
-    __shared__ double Uj[kTile][kHalf + 1];
-    __shared__ double Dk[kTile];
     const int64_t i0 = bi * kTile, j0 = bj * kTile;
-    if (threadIdx.x < kTile) Dk[threadIdx.x] = D[k0 + threadIdx.x];
+    if (threadIdx.x < kTile) L.Dk[threadIdx.x] = D[k0 + threadIdx.x];
     const int tr = threadIdx.x / 16, tc = threadIdx.x % 16;
     double acc[4][4];
 #pragma unroll
@@ -196,17 +208,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
         __syncthreads();                                          // the previous half is used
         for (int t = threadIdx.x; t < kTile * kHalf; t += 256) {
             const int kk = t / kTile, r = t % kTile;              // coalesced over r
-            Ui[r][kk] = Uc[(k0 + h + kk) * n + i0 + r];
-            Uj[r][kk] = Uc[(k0 + h + kk) * n + j0 + r];
+            L.Ui[r][kk] = Uc[(k0 + h + kk) * n + i0 + r];
+            L.Uj[r][kk] = Uc[(k0 + h + kk) * n + j0 + r];
         }
         __syncthreads();
         for (int kk = kHalf - 1; kk >= 0; --kk) {
             double ua[4], ub[4];
 #pragma unroll
-            for (int a = 0; a < 4; ++a) ua[a] = Ui[tr + 16 * a][kk];
+            for (int a = 0; a < 4; ++a) ua[a] = L.Ui[tr + 16 * a][kk];
 #pragma unroll
-            for (int b = 0; b < 4; ++b) ub[b] = Uj[tc + 16 * b][kk];
-            const double dk = Dk[h + kk];
+            for (int b = 0; b < 4; ++b) ub[b] = L.Uj[tc + 16 * b][kk];
+            const double dk = L.Dk[h + kk];
 #pragma unroll
             for (int a = 0; a < 4; ++a)
 #pragma unroll
@@ -220,6 +232,31 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
             const int64_t i = i0 + tr + 16 * a, j = j0 + tc + 16 * b;
             if (i <= j) Uc[j * n + i] = acc[a][b];
         }
+}
+
+// Tiles (bi, bj0 + blockIdx.x), bi = blockIdx.y.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void factor_trailing_kernel(
+        double* __restrict__ Uc, const double* __restrict__ D, int64_t n, int64_t k0, int64_t bj0) {
+    __shared__ FTrailLds L;
+    factor_trailing_body(Uc, D, n, k0, blockIdx.y, bj0 + blockIdx.x, L);
+}
+
+// Look-ahead: the next diagonal block [kd, kd + 64) (workgroup 0, once the column of tiles it
+// needs has been updated) beside the rest of the current block's trailing update, tiles with
+// bj < nb (the other workgroups, nb x nb of them).  The two touch disjoint elements.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void factor_lookahead_kernel(
+        double* __restrict__ Uc, double* __restrict__ D, int64_t n, int64_t k0, int64_t nb, int64_t kd,
+        int* __restrict__ status) {
+    __shared__ union {
+        DiagLds d;
+        FTrailLds t;
+    } L;
+    if (blockIdx.x == 0) {
+        factor_diag_body(Uc, D, n, kd, status, L.d);
+    } else {
+        const int64_t idx = blockIdx.x - 1;
+        factor_trailing_body(Uc, D, n, k0, idx / nb, idx % nb, L.t);
+    }
 }
 
 // ---- quantize -----------------------------------------------------------------------------
@@ -256,35 +293,36 @@ __device__ __forceinline__ double quad_bcast(double v) {
 // columns a > b.  Every value thus receives its terms b = a0, a0 + 1, ... in ascending order,
 // as the sequential definition adds them.  The row's weights and scale bytes are staged in LDS
 // (read by the four lanes alike), U's tile block too.
+struct TileLds {
+    double T[kTile][kTile];        // T[b][a] = U_{a0+b, a0+a}
+    float wsv[kTile][kTile + 1];   // wsv[rr][a]: the weight of tile column a, row rr
+    uint8_t scs[kTile][kTile];     // scs[rr][a]: its block's scale code
+    int pc[kTile];
+};
+
 template <typename In>
-__global__ __launch_bounds__(4 * kTile) void tile_kernel(const In* __restrict__ w, const int* __restrict__ perm,
-                                                         const double* __restrict__ Uc,
-                                                         const uint8_t* __restrict__ scales,
-                                                         const float* __restrict__ tensor_scale,
-                                                         int64_t rows, int64_t n, int block, int64_t a0,
-                                                         const double* __restrict__ X,
-                                                         double* __restrict__ Et,
-                                                         uint8_t* __restrict__ codes) {
-    __shared__ double T[kTile][kTile];      // T[b][a] = U_{a0+b, a0+a}
-    __shared__ float wsv[kTile][kTile + 1]; // wsv[rr][a]: the weight of tile column a, row rr
-    __shared__ uint8_t scs[kTile][kTile];   // scs[rr][a]: its block's scale code
-    __shared__ int pc[kTile];
+__device__ __forceinline__ void tile_body(const In* __restrict__ w, const int* __restrict__ perm,
+                                          const double* __restrict__ Uc, const uint8_t* __restrict__ scales,
+                                          const float* __restrict__ tensor_scale, int64_t rows, int64_t n,
+                                          int block, int64_t a0, const double* __restrict__ X,
+                                          double* __restrict__ Et, uint8_t* __restrict__ codes,
+                                          int64_t rblock, TileLds& L) {
     const int tid = threadIdx.x;
     for (int t = tid; t < kTile * kTile; t += 4 * kTile) {
         const int a = t / kTile, b = t % kTile;                   // coalesced over b
-        T[b][a] = Uc[(a0 + a) * n + a0 + b];
+        L.T[b][a] = Uc[(a0 + a) * n + a0 + b];
     }
-    if (tid < kTile) pc[tid] = perm[a0 + tid];
+    if (tid < kTile) L.pc[tid] = perm[a0 + tid];
     __syncthreads();
     const int rr = tid >> 2, p = tid & 3;
-    const int64_t r = (int64_t)blockIdx.x * kTile + rr;
+    const int64_t r = rblock * kTile + rr;
     if (r >= rows) return;                   // whole quads: the broadcasts stay inside live rows
     const int64_t nb = n / block;
 #pragma unroll
     for (int j = 0; j < 16; ++j) {           // this lane's share of the row's weights and scales
-        const int a = 16 * p + j, c = pc[a];
-        wsv[rr][a] = load_w<In>(w, r * n + c);
-        scs[rr][a] = scales[r * nb + c / block];
+        const int a = 16 * p + j, c = L.pc[a];
+        L.wsv[rr][a] = load_w<In>(w, r * n + c);
+        L.scs[rr][a] = scales[r * nb + c / block];
     }
     double x[16];
 #pragma unroll
@@ -298,35 +336,51 @@ __global__ __launch_bounds__(4 * kTile) void tile_kernel(const In* __restrict__ 
         constexpr int b = decltype(bc)::value, pb = b / 16, jb = b % 16;
         const double xb = quad_bcast<pb>(x[jb]);
         const float y = __fdiv_rn(__double2float_rn(xb), S);
-        const double s = e4m3_f64(scs[rr][b]);
+        const double s = e4m3_f64(L.scs[rr][b]);
         const int k = round_fp4_index(fabs((double)y), s);
         double wq = e2m1_value(k) * s * Sd;
         const bool neg = signbit(y);
         if (neg) wq = -wq;
-        const double e = (double)wsv[rr][b] - wq;
+        const double e = (double)L.wsv[rr][b] - wq;
         if (p == pb) {
-            codes[r * n + pc[b]] = (uint8_t)((neg ? 8 : 0) | k);
+            codes[r * n + L.pc[b]] = (uint8_t)((neg ? 8 : 0) | k);
             Et[r * kTile + b] = e;
         }
 #pragma unroll
         for (int j = 0; j < 16; ++j)
-            if (16 * p + j > b) x[j] = x[j] + e * T[b][16 * p + j];
+            if (16 * p + j > b) x[j] = x[j] + e * L.T[b][16 * p + j];
     };
     for_each_index(column, std::make_integer_sequence<int, kTile>());
 }
 
-// X[r][k] += sum over the tile's b (in order) of Et[r][b] * U_{a0+b, k}, for k >= a0 + 64:
-// one 64 x 64 output block per workgroup, 4 x 4 values per lane, the terms staged 32 at a time
-// (so that four workgroups fit a CU's LDS: four waves per SIMD to issue the binary64 chains).
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void trailing_kernel(const double* __restrict__ Et,
-                                                       const double* __restrict__ Uc,
-                                                       int64_t rows, int64_t n, int64_t a0,
-                                                       double* __restrict__ X) {
-    constexpr int kHalf = kTile / 2;
-    __shared__ double Es[kTile][kHalf + 1];    // Es[row][b]
-    __shared__ double Us[kHalf][kTile + 1];    // Us[b][col]
-    const int64_t r0 = (int64_t)blockIdx.y * kTile;
-    const int64_t k0 = a0 + kTile + (int64_t)blockIdx.x * kTile;
+template <typename In>
+__global__ __launch_bounds__(4 * kTile) void tile_kernel(const In* __restrict__ w, const int* __restrict__ perm,
+                                                         const double* __restrict__ Uc,
+                                                         const uint8_t* __restrict__ scales,
+                                                         const float* __restrict__ tensor_scale,
+                                                         int64_t rows, int64_t n, int block, int64_t a0,
+                                                         const double* __restrict__ X,
+                                                         double* __restrict__ Et,
+                                                         uint8_t* __restrict__ codes) {
+    __shared__ TileLds L;
+    tile_body<In>(w, perm, Uc, scales, tensor_scale, rows, n, block, a0, X, Et, codes, blockIdx.x, L);
+}
+
+// X[r][k] += sum over the tile's b (in order) of Et[r][b] * U_{a0+b, k}, for k in [kstart,
+// kend): one 64 x 64 output block (column block bx, row block by) per workgroup, 4 x 4 values
+// per lane, the terms staged 32 at a time (so that four workgroups fit a CU's LDS: four waves
+// per SIMD to issue the binary64 chains).
+struct QTrailLds {
+    double Es[kTile][kHalf + 1];   // Es[row][b]
+    double Us[kHalf][kTile + 1];   // Us[b][col]
+};
+
+__device__ __forceinline__ void trailing_body(const double* __restrict__ Et, const double* __restrict__ Uc,
+                                              int64_t rows, int64_t n, int64_t a0, int64_t kstart,
+                                              int64_t kend, double* __restrict__ X, int64_t bx,
+                                              int64_t by, QTrailLds& L) {
+    const int64_t r0 = by * kTile;
+    const int64_t k0 = kstart + bx * kTile;
     const int tr = threadIdx.x / 16, tc = threadIdx.x % 16;      // 16 x 16 lanes, 4 x 4 each
     double acc[4][4];
 #pragma unroll
@@ -334,23 +388,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void t
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int64_t r = r0 + tr + 16 * i, k = k0 + tc + 16 * j;
-            acc[i][j] = (r < rows && k < n) ? X[r * n + k] : 0.0;
+            acc[i][j] = (r < rows && k < kend) ? X[r * n + k] : 0.0;
         }
     for (int h = 0; h < kTile; h += kHalf) {
         __syncthreads();                                          // the previous half is used
         for (int t = threadIdx.x; t < kTile * kHalf; t += 256) {
             const int rr = t / kHalf, b = t % kHalf;              // coalesced over b
-            Es[rr][b] = r0 + rr < rows ? Et[(r0 + rr) * kTile + h + b] : 0.0;
+            L.Es[rr][b] = r0 + rr < rows ? Et[(r0 + rr) * kTile + h + b] : 0.0;
             const int cc = t / kHalf, bb = t % kHalf;
-            Us[bb][cc] = k0 + cc < n ? Uc[(k0 + cc) * n + a0 + h + bb] : 0.0;
+            L.Us[bb][cc] = k0 + cc < kend ? Uc[(k0 + cc) * n + a0 + h + bb] : 0.0;
         }
         __syncthreads();
         for (int b = 0; b < kHalf; ++b) {
             double e[4], u[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) e[i] = Es[tr + 16 * i][b];
+            for (int i = 0; i < 4; ++i) e[i] = L.Es[tr + 16 * i][b];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) u[j] = Us[b][tc + 16 * j];
+            for (int j = 0; j < 4; ++j) u[j] = L.Us[b][tc + 16 * j];
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -362,8 +416,39 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void t
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int64_t r = r0 + tr + 16 * i, k = k0 + tc + 16 * j;
-            if (r < rows && k < n) X[r * n + k] = acc[i][j];
+            if (r < rows && k < kend) X[r * n + k] = acc[i][j];
         }
+}
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void trailing_kernel(
+        const double* __restrict__ Et, const double* __restrict__ Uc, int64_t rows, int64_t n, int64_t a0,
+        int64_t kstart, int64_t kend, double* __restrict__ X) {
+    __shared__ QTrailLds L;
+    trailing_body(Et, Uc, rows, n, a0, kstart, kend, X, blockIdx.x, blockIdx.y, L);
+}
+
+// Look-ahead: the next tile (workgroups 0 .. ntile-1, its errors into Etn) beside the rest of
+// the current tile's trailing update, columns [kstart, n) with the current tile's errors Etc
+// (the other workgroups, ncb column blocks per row block).  The next tile's columns already
+// hold every earlier term; the two touch disjoint values.
+template <typename In>
+__global__ __launch_bounds__(4 * kTile) __attribute__((amdgpu_waves_per_eu(3))) void tile_lookahead_kernel(
+        const In* __restrict__ w, const int* __restrict__ perm, const double* __restrict__ Uc,
+        const uint8_t* __restrict__ scales, const float* __restrict__ tensor_scale, int64_t rows,
+        int64_t n, int block, int64_t a0n, double* __restrict__ X, double* __restrict__ Etn,
+        uint8_t* __restrict__ codes, int64_t ntile, const double* __restrict__ Etc, int64_t a0c,
+        int64_t kstart, int64_t ncb) {
+    __shared__ union {
+        TileLds t;
+        QTrailLds q;
+    } L;
+    if ((int64_t)blockIdx.x < ntile) {
+        tile_body<In>(w, perm, Uc, scales, tensor_scale, rows, n, block, a0n, X, Etn, codes, blockIdx.x,
+                      L.t);
+    } else {
+        const int64_t idx = blockIdx.x - ntile;
+        trailing_body(Etc, Uc, rows, n, a0c, kstart, n, X, idx % ncb, idx / ncb, L.q);
+    }
 }
 
 __global__ __launch_bounds__(256) void pack_kernel(const uint8_t* __restrict__ codes, int64_t npairs,
@@ -391,7 +476,7 @@ Layout layout_of(int64_t rows, int64_t n) {
     l.D = o;      o = align256(o + (size_t)n * sizeof(double));
     l.Uc = o;     o = align256(o + (size_t)n * n * sizeof(double));
     l.X = o;      o = align256(o + (size_t)rows * n * sizeof(double));
-    l.Et = o;     o = align256(o + (size_t)rows * kTile * sizeof(double));
+    l.Et = o;     o = align256(o + (size_t)2 * rows * kTile * sizeof(double));   // two tiles in turn
     l.codes = o;  o = align256(o + (size_t)rows * n);
     l.total = o;
     return l;
@@ -421,25 +506,38 @@ int run_ldlq(const void* wv, int64_t rows, int64_t n, int block, const double* H
     if (hipGetLastError() != hipSuccess) return NVFP4_ERR_HIP;
     hipLaunchKernelGGL(init_a_kernel, dim3(blocks_for(n * n, 256)), dim3(256), 0, st, H, perm, lambda,
                        n, Uc);
-    for (int64_t k0 = n - kTile; k0 >= 0; k0 -= kTile) {
-        hipLaunchKernelGGL(factor_diag_kernel, dim3(1), dim3(4 * kTile), 0, st, Uc, D, n, k0, status);
-        if (k0 > 0) {
-            hipLaunchKernelGGL(factor_panel_kernel, dim3(blocks_for(k0, kTile)), dim3(4 * kTile), 0, st, Uc,
-                               D, n, k0);
-            const unsigned tiles = (unsigned)(k0 / kTile);
-            hipLaunchKernelGGL(factor_trailing_kernel, dim3(tiles, tiles), dim3(256), 0, st, Uc, D, n, k0);
-        }
+    // factor, from the last block: its diagonal block, then per block the panel above it, the
+    // column of tiles the next diagonal block and panel need, and then the next diagonal block
+    // beside the rest of the trailing update (look-ahead)
+    hipLaunchKernelGGL(factor_diag_kernel, dim3(1), dim3(4 * kTile), 0, st, Uc, D, n, n - kTile, status);
+    for (int64_t k0 = n - kTile; k0 > 0; k0 -= kTile) {
+        hipLaunchKernelGGL(factor_panel_kernel, dim3(blocks_for(k0, kTile)), dim3(4 * kTile), 0, st, Uc, D,
+                           n, k0);
+        const int64_t nb = k0 / kTile - 1;                         // the next block's tile column
+        hipLaunchKernelGGL(factor_trailing_kernel, dim3(1, (unsigned)(nb + 1)), dim3(256), 0, st, Uc, D, n,
+                           k0, nb);
+        hipLaunchKernelGGL(factor_lookahead_kernel, dim3((unsigned)(1 + nb * nb)), dim3(256), 0, st, Uc, D,
+                           n, k0, nb > 0 ? nb : 1, k0 - kTile, status);
         if (hipGetLastError() != hipSuccess) return NVFP4_ERR_HIP;
     }
     hipLaunchKernelGGL(init_x_kernel<In>, dim3(blocks_for(rows * n, 256)), dim3(256), 0, st, w, perm,
                        rows, n, X);
-    for (int64_t a0 = 0; a0 < n; a0 += kTile) {
-        hipLaunchKernelGGL(tile_kernel<In>, dim3(blocks_for(rows, kTile)), dim3(4 * kTile), 0, st, w, perm, Uc,
-                           scales, S, rows, n, block, a0, X, Et, codes);
-        const int64_t rest = n - a0 - kTile;
-        if (rest > 0)
-            hipLaunchKernelGGL(trailing_kernel, dim3(blocks_for(rest, kTile), blocks_for(rows, kTile)),
-                               dim3(256), 0, st, Et, Uc, rows, n, a0, X);
+    // quantize: tile 0, then per tile the next tile's columns, and then the next tile beside
+    // the rest of the trailing update (look-ahead); the tiles' errors alternate between two
+    // buffers
+    const unsigned rblocks = blocks_for(rows, kTile);
+    hipLaunchKernelGGL(tile_kernel<In>, dim3(rblocks), dim3(4 * kTile), 0, st, w, perm, Uc, scales, S,
+                       rows, n, block, (int64_t)0, X, Et, codes);
+    for (int64_t a0 = 0; a0 + kTile < n; a0 += kTile) {
+        double* Etc = Et + ((a0 / kTile) & 1) * rows * kTile;
+        double* Etn = Et + (((a0 / kTile) + 1) & 1) * rows * kTile;
+        hipLaunchKernelGGL(trailing_kernel, dim3(1, rblocks), dim3(256), 0, st, Etc, Uc, rows, n, a0,
+                           a0 + kTile, a0 + 2 * kTile, X);
+        const int64_t rest = n - (a0 + 2 * kTile);                  // columns past the next tile
+        const int64_t ncb = (rest + kTile - 1) / kTile;
+        hipLaunchKernelGGL(tile_lookahead_kernel<In>, dim3((unsigned)(rblocks + ncb * rblocks)),
+                           dim3(4 * kTile), 0, st, w, perm, Uc, scales, S, rows, n, block, a0 + kTile, X, Etn,
+                           codes, (int64_t)rblocks, Etc, a0, a0 + 2 * kTile, ncb > 0 ? ncb : 1);
         if (hipGetLastError() != hipSuccess) return NVFP4_ERR_HIP;
     }
     hipLaunchKernelGGL(pack_kernel, dim3(blocks_for(rows * n / 2, 256)), dim3(256), 0, st, codes,
