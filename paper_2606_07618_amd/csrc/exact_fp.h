@@ -18,15 +18,17 @@ __device__ __forceinline__ double e2m1_mid(int k) {
     return (double)(int)((quads >> (8 * k)) & 0xFFu) * 0.25;
 }
 
+// E2M1 magnitude of index k (0..7): twice the values, 0 1 2 3 4 6 8 12, are the nibbles of one
+// 32-bit constant (no branch).
 __device__ __forceinline__ double e2m1_value(int k) {
-    return k == 0 ? 0.0 : k == 1 ? 0.5 : k == 2 ? 1.0 : k == 3 ? 1.5
-         : k == 4 ? 2.0 : k == 5 ? 3.0 : k == 6 ? 4.0 : 6.0;
+    return (double)((0xC8643210u >> (4 * k)) & 15u) * 0.5;
 }
 
-// E4M3 code c = a * 8 + b (0..126): 2^(a - 7) (1 + b/8) for a > 0, 2^-6 (b/8) for a = 0.
+// E4M3 code c = a * 8 + b (0..126): 2^(a - 7) (1 + b/8) for a > 0, 2^-6 (b/8) for a = 0, i.e.
+// (8 + b) 2^(a - 10) and b 2^-9 (no branch).
 __device__ __forceinline__ double e4m3_f64(int c) {
     const int a = c >> 3, b = c & 7;
-    return a ? ldexp(1.0 + 0.125 * b, a - 7) : ldexp(0.125 * b, -6);
+    return ldexp((double)(a ? 8 + b : b), (a ? a : 1) - 10);
 }
 
 // Index of the E2M1 value nearest to a / s (a >= 0, s > 0): the number of midpoints m_j with

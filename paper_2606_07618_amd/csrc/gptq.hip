@@ -51,6 +51,22 @@ __device__ __forceinline__ float load_w<uint16_t>(const uint16_t* w, int64_t i) 
     return __uint_as_float((uint32_t)w[i] << 16);
 }
 
+// f(integral_constant<int, B>) for B = 0, 1, ... in order (the calls unrolled at compile time).
+template <typename F, int... B>
+__device__ __forceinline__ void for_each_index(F&& f, std::integer_sequence<int, B...>) {
+    (f(std::integral_constant<int, B>()), ...);
+}
+
+// Lane l of a quad broadcasts v to the quad's four lanes (a DPP quad permutation).
+template <int L>
+__device__ __forceinline__ double quad_bcast(double v) {
+    constexpr int ctrl = L * 0x55;                    // quad_perm(L, L, L, L)
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, ctrl, 0xF, 0xF, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), ctrl, 0xF, 0xF, false);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
 // ---- column order and damping ------------------------------------------------------------
 
 __global__ __launch_bounds__(256) void diag_kernel(const double* __restrict__ H, int64_t n,
@@ -99,41 +115,91 @@ __global__ __launch_bounds__(256) void init_a_kernel(const double* __restrict__ 
     Uc[t] = v;
 }
 
-// The diagonal block [k0, k0 + 64): its D and its U, column by column from the last, in LDS.
-// The block's own 64 columns, right-looking: at step kk (from the last) D_kk is the updated
+// The diagonal block [k0, k0 + 64): its D and its U, column by column from the last.  The
+// block's own 64 columns, right-looking: at step kk (from the last) D_kk is the updated
 // diagonal, U_i,kk = A_i,kk / D_kk for i < kk, and every A_ij (i <= j < kk) then loses
 // (U_ik U_jk) D_k, so each element receives its terms k = 63, 62, ... in the order the
-// column-by-column definition sums them.  Four threads per row, each a quarter of its
-// columns, so that a step's updates run in parallel.
-struct DiagLds {
-    double Ab[kTile][kTile + 1];   // Ab[ii][jj]: A, then U, of (k0 + ii, k0 + jj)
+// column-by-column definition sums them.  A quad of threads per row, thread q holding the
+// row's values of columns 4m + q in registers; column kk of U goes through LDS.  One barrier
+// per step: after its updates every thread forms D_(kk-1) itself from the value its owner
+// published before the step (the owner's own update, the same operations), so the threads
+// holding column kk - 1 can divide at once and publish that column for the next step.
+struct alignas(16) DiagLds {
+    double col[2][kTile];          // col[kk & 1][16 (i & 3) + (i >> 2)] = U_{k0+i, k0+kk}
+    double pre[2];                 // pre[kk & 1]: A_(kk-1),(kk-1) before step kk
     double Db[kTile];
 };
+
+__device__ __forceinline__ int quad_slot(int j) { return 16 * (j & 3) + (j >> 2); }
 
 __device__ __forceinline__ void factor_diag_body(double* __restrict__ Uc, double* __restrict__ D,
                                                  int64_t n, int64_t k0, int* __restrict__ status,
                                                  DiagLds& L) {
     const int tid = threadIdx.x;
-    for (int t = tid; t < kTile * kTile; t += 4 * kTile) {
-        const int jj = t / kTile, ii = t % kTile;                 // coalesced over ii
-        L.Ab[ii][jj] = Uc[(k0 + jj) * n + k0 + ii];
+    const int i = tid >> 2, q = tid & 3;
+    double v[16];                            // A (then U) of (k0 + i, k0 + 4m + q)
+#pragma unroll
+    for (int m = 0; m < 16; ++m) v[m] = Uc[(k0 + 4 * m + q) * n + k0 + i];
+    // column 63: its diagonal, then its U, and A_62,62 for step 63
+    if (i == kTile - 1 && q == 3) L.Db[kTile - 1] = v[15];
+    __syncthreads();
+    {
+        const double d = L.Db[kTile - 1];
+        const double u = v[15] / d;
+        if (q == 3 && i < kTile - 1) {
+            v[15] = u;
+            L.col[1][quad_slot(i)] = u;
+        }
+        if (i == kTile - 2 && q == 2) L.pre[1] = v[15];
     }
     __syncthreads();
-    const int i = tid >> 2, q = tid & 3;
-    for (int kk = kTile - 1; kk >= 0; --kk) {
-        const double d = L.Ab[kk][kk];
-        if (q == 0 && i < kk) L.Ab[i][kk] = L.Ab[i][kk] / d;       // U_i,kk
-        if (tid == 0) L.Db[kk] = d;
-        __syncthreads();
-        if (i < kk) {
-            const double ui = L.Ab[i][kk];
-            for (int j = i + q; j < kk; j += 4) L.Ab[i][j] = L.Ab[i][j] - (ui * L.Ab[j][kk]) * d;
+    auto step = [&](auto kc) {
+        constexpr int kk = kTile - 1 - decltype(kc)::value, par = kk & 1;
+        const double d = L.Db[kk];
+        const double* c = &L.col[par][0];
+        const double ui = c[quad_slot(i)];
+        const double* cq = c + 16 * q;
+        // the updates of this step: A_ij, i <= j = 4m + q < kk, in two halves of eight columns
+        // (U values read together first; each new value formed in every lane, then selected)
+#pragma unroll
+        for (int h = 0; h < 16; h += 8) {
+            double uj[8];
+#pragma unroll
+            for (int m = 0; m < 8; ++m) uj[m] = 4 * (h + m) < kk ? cq[h + m] : 0.0;
+#pragma unroll
+            for (int m = 0; m < 8; ++m) {
+                if (4 * (h + m) < kk) {
+                    double nv = v[h + m] - (ui * uj[m]) * d;
+                    asm volatile("" : "+v"(nv));
+                    const int j = 4 * (h + m) + q;
+                    v[h + m] = (j >= i && j < kk) ? nv : v[h + m];
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
         }
-        __syncthreads();
-    }
-    for (int t = tid; t < kTile * kTile; t += 4 * kTile) {
-        const int jj = t / kTile, ii = t % kTile;
-        if (ii < jj) Uc[(k0 + jj) * n + k0 + ii] = L.Ab[ii][jj];
+        if constexpr (kk >= 1) {
+            constexpr int k1 = kk - 1, q1 = k1 & 3, m1 = k1 >> 2;
+            // D_(kk-1): its owner's update of this step, formed by every thread alike
+            const double u1 = c[quad_slot(k1)];
+            const double d1 = L.pre[par] - (u1 * u1) * d;
+            const double u = v[m1] / d1;
+            if (q == q1 && i < k1) {
+                v[m1] = u;
+                L.col[par ^ 1][quad_slot(i)] = u;
+            }
+            if (tid == 0) L.Db[k1] = d1;
+            if constexpr (kk >= 2) {
+                constexpr int k2 = kk - 2, q2 = k2 & 3, m2 = k2 >> 2;
+                if (i == k2 && q == q2) L.pre[par ^ 1] = v[m2];
+            }
+            __syncthreads();
+        }
+    };
+    for_each_index(step, std::make_integer_sequence<int, kTile>());
+#pragma unroll
+    for (int m = 0; m < 16; ++m) {
+        const int j = 4 * m + q;
+        if (i < j) Uc[(k0 + j) * n + k0 + i] = v[m];
     }
     if (tid < kTile) {
         const double d = L.Db[tid];
@@ -148,40 +214,49 @@ __global__ __launch_bounds__(4 * kTile) void factor_diag_kernel(double* __restri
     factor_diag_body(Uc, D, n, k0, status, L);
 }
 
-// Rows above the block (i < k0), 64 per workgroup, four threads per row: U_ij for the block's
-// columns, each row a triangular solve from the block's last column, right-looking: at step
-// kk the row's value of column kk is final, U_i,kk = A_i,kk / D_kk, and each of the row's
-// columns j < kk loses (U_i,kk U_j,kk) D_kk, the threads of the row taking every fourth
-// column.  So each value receives its terms kk = 63, 62, ... in the order the column-by-column
-// definition sums them.  The rows' starting values are loaded together first.
+// Rows above the block (i < k0), 64 per workgroup, a quad of lanes per row: lane q holds the
+// row's values of block columns 4m + q in registers.  Each row is a triangular solve from the
+// block's last column, right-looking: at step kk the row's value of column kk is final,
+// U_i,kk = A_i,kk / D_kk (broadcast in the quad), and each of the row's columns j < kk loses
+// (U_i,kk U_j,kk) D_kk.  So each value receives its terms kk = 63, 62, ... in the order the
+// column-by-column definition sums them.  A step holds no branch; the block's U and D are
+// staged in LDS (each lane's columns of a U row contiguous).
 __global__ __launch_bounds__(4 * kTile) void factor_panel_kernel(double* __restrict__ Uc,
                                                                  const double* __restrict__ D, int64_t n,
                                                                  int64_t k0) {
-    __shared__ double Ub[kTile][kTile + 1];   // Ub[jj][kk] = U_{k0+jj, k0+kk}, jj < kk
-    __shared__ double ui[kTile][kTile + 1];   // ui[rr][kk]: A, then U, of (i0 + rr, k0 + kk)
+    __shared__ double Ub[kTile][kTile];       // Ub[kk][16 q + m] = U_{k0+4m+q, k0+kk}
     __shared__ double Db[kTile];
     const int tid = threadIdx.x;
     const int64_t i0 = (int64_t)blockIdx.x * kTile;
     for (int t = tid; t < kTile * kTile; t += 4 * kTile) {
-        const int kk = t / kTile, m = t % kTile;                  // coalesced over m
-        Ub[m][kk] = Uc[(k0 + kk) * n + k0 + m];
-        if (i0 + m < k0) ui[m][kk] = Uc[(k0 + kk) * n + i0 + m];
+        const int kk = t / kTile, jj = t % kTile;                 // coalesced over jj
+        Ub[kk][quad_slot(jj)] = Uc[(k0 + kk) * n + k0 + jj];
     }
     if (tid < kTile) Db[tid] = D[k0 + tid];
-    __syncthreads();
     const int rr = tid >> 2, q = tid & 3;
     const int64_t i = i0 + rr;
-    if (i >= k0) return;                     // whole quads; rows share nothing
-    for (int kk = kTile - 1; kk >= 0; --kk) {
-        const double dk = Db[kk];
-        const double u = ui[rr][kk] / dk;    // the four threads alike
-        if (q == 0) Uc[(k0 + kk) * n + i] = u;
-        for (int j = q; j < kk; j += 4) ui[rr][j] = ui[rr][j] - (u * Ub[j][kk]) * dk;
-        // the row's next column (updated by one of its threads) is read by all four next
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    double v[16];
+    if (i < k0) {
+#pragma unroll
+        for (int m = 0; m < 16; ++m) v[m] = Uc[(k0 + 4 * m + q) * n + i];
     }
+    __syncthreads();
+    if (i >= k0) return;                     // whole quads; rows share nothing
+    const double* Up = &Ub[0][16 * q];
+    auto step = [&](auto kc) {
+        constexpr int kk = kTile - 1 - decltype(kc)::value, qk = kk & 3, mk = kk >> 2;
+        const double dk = Db[kk];
+        const double u = quad_bcast<qk>(v[mk]) / dk;
+        Uc[(k0 + kk) * n + i] = u;           // the quad's four lanes store the same value
+#pragma unroll
+        for (int m = 0; m < 16; ++m) {
+            if (4 * m < kk) {                // some lane of the quad holds a column before kk
+                const double nv = v[m] - (u * Up[kk * kTile + m]) * dk;
+                v[m] = (4 * m + 3 < kk || q < kk - 4 * m) ? nv : v[m];
+            }
+        }
+    };
+    for_each_index(step, std::make_integer_sequence<int, kTile>());
 }
 
 // A_ij -= sum over the block's k, downwards, of (U_ik U_jk) D_k for i <= j < k0: one 64 x 64
@@ -247,7 +322,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
 // Look-ahead: the next diagonal block [kd, kd + 64) (workgroup 0, once the column of tiles it
 // needs has been updated) beside the rest of the current block's trailing update, tiles with
 // bj < nb (the other workgroups, nb x nb of them).  The two touch disjoint elements.
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void factor_lookahead_kernel(
+__global__ __launch_bounds__(256) void factor_lookahead_kernel(
         double* __restrict__ Uc, double* __restrict__ D, int64_t n, int64_t k0, int64_t nb, int64_t kd,
         int* __restrict__ status) {
     __shared__ union {
@@ -273,31 +348,18 @@ __global__ __launch_bounds__(256) void init_x_kernel(const In* __restrict__ w, c
     X[t] = (double)load_w<In>(w, r * n + perm[a]);
 }
 
-// f(integral_constant<int, B>) for B = 0, 1, ... in order (the calls unrolled at compile time).
-template <typename F, int... B>
-__device__ __forceinline__ void for_each_index(F&& f, std::integer_sequence<int, B...>) {
-    (f(std::integral_constant<int, B>()), ...);
-}
-
-// Lane l of a quad broadcasts v to the quad's four lanes (a DPP quad permutation).
-template <int L>
-__device__ __forceinline__ double quad_bcast(double v) {
-    constexpr int ctrl = L * 0x55;                    // quad_perm(L, L, L, L)
-    const uint64_t b = (uint64_t)__double_as_longlong(v);
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, ctrl, 0xF, 0xF, false);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), ctrl, 0xF, 0xF, false);
-    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
-}
-
 // One tile of 64 columns, right-looking, four lanes (a quad) per row and 64 rows per
-// workgroup: lane p of a quad holds the running values of tile columns 16p .. 16p + 15 in
+// workgroup: lane p of a quad holds the running values of tile columns 4j + p, j = 0..15, in
 // registers.  Column b's value is broadcast to the quad, which quantizes it (every lane the
 // same operations, so the same error), and each lane then adds error_b * U_b,a to each of its
 // columns a > b.  Every value thus receives its terms b = a0, a0 + 1, ... in ascending order,
 // as the sequential definition adds them.  The row's weights and scale bytes are staged in LDS
-// (read by the four lanes alike), U's tile block too.
-struct TileLds {
-    double T[kTile][kTile];        // T[b][a] = U_{a0+b, a0+a}
+// (read by the four lanes alike), U's tile block too, each lane's columns of a U row
+// contiguous.  A column's work holds no branch: its scale, weight, midpoint products and U
+// values do not depend on the running value, so they are read and formed ahead of the chain
+// value -> quotient -> E2M1 index -> error -> the next column's value that bounds the walk.
+struct alignas(16) TileLds {
+    double T[kTile][kTile];        // T[b][16 p + j] = U_{a0+b, a0+4j+p}
     float wsv[kTile][kTile + 1];   // wsv[rr][a]: the weight of tile column a, row rr
     uint8_t scs[kTile][kTile];     // scs[rr][a]: its block's scale code
     int pc[kTile];
@@ -313,7 +375,7 @@ __device__ __forceinline__ void tile_body(const In* __restrict__ w, const int* _
     const int tid = threadIdx.x;
     for (int t = tid; t < kTile * kTile; t += 4 * kTile) {
         const int a = t / kTile, b = t % kTile;                   // coalesced over b
-        L.T[b][a] = Uc[(a0 + a) * n + a0 + b];
+        L.T[b][16 * (a & 3) + (a >> 2)] = Uc[(a0 + a) * n + a0 + b];
     }
     if (tid < kTile) L.pc[tid] = perm[a0 + tid];
     __syncthreads();
@@ -329,29 +391,49 @@ __device__ __forceinline__ void tile_body(const In* __restrict__ w, const int* _
     }
     double x[16];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) x[j] = X[r * n + a0 + 16 * p + j];
+    for (int j = 0; j < 16; ++j) x[j] = X[r * n + a0 + 4 * j + p];
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");   // the quad's LDS stores, then reads
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     const float S = tensor_scale[0];
-    const double Sd = (double)S;
+    const double halfS = 0.5 * (double)S;
+    const double* Tp = &L.T[0][16 * p];
+    uint8_t* crow = codes + r * n;
+    double* erow = Et + r * kTile;
     auto column = [&](auto bc) {
-        constexpr int b = decltype(bc)::value, pb = b / 16, jb = b % 16;
+        constexpr int b = decltype(bc)::value, pb = b & 3, jb = b >> 2;
+        // independent of the running values
+        const int code = L.scs[rr][b];
+        const double s = e4m3_f64(code);
+        const double wv = (double)L.wsv[rr][b];
+        const double gscale = s * halfS;     // E2M1(k) s S = (2 E2M1(k)) (s S / 2), all exact
+        double m[7];                          // the midpoints times s (exact: <= 7 significant bits)
+#pragma unroll
+        for (int jm = 0; jm < 7; ++jm) m[jm] = e2m1_mid(jm) * s;
+        // the chain
         const double xb = quad_bcast<pb>(x[jb]);
         const float y = __fdiv_rn(__double2float_rn(xb), S);
-        const double s = e4m3_f64(L.scs[rr][b]);
-        const int k = round_fp4_index(fabs((double)y), s);
-        double wq = e2m1_value(k) * s * Sd;
-        const bool neg = signbit(y);
-        if (neg) wq = -wq;
-        const double e = (double)L.wsv[rr][b] - wq;
-        if (p == pb) {
-            codes[r * n + L.pc[b]] = (uint8_t)((neg ? 8 : 0) | k);
-            Et[r * kTile + b] = e;
-        }
+        const double ay = fabs((double)y);
+        // index of the nearest E2M1 value: the midpoints passed, a tie counting only toward an
+        // even index (midpoints 1, 3, 5); none for a zero scale
+        int k = 0;
 #pragma unroll
-        for (int j = 0; j < 16; ++j)
-            if (16 * p + j > b) x[j] = x[j] + e * L.T[b][16 * p + j];
+        for (int jm = 0; jm < 7; ++jm) k += ((jm & 1) ? ay >= m[jm] : ay > m[jm]) ? 1 : 0;
+        k = code == 0 ? 0 : k;
+        const bool neg = signbit(y);
+        const double wq = (double)((0xC8643210u >> (4 * k)) & 15u) * gscale;
+        const double e = wv - (neg ? -wq : wq);
+        // the quad's four lanes store the same code and error
+        crow[L.pc[b]] = (uint8_t)((neg ? 8 : 0) | k);
+        erow[b] = e;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            if (4 * j + 3 > b) {             // some lane of the quad holds a column past b
+                const double v = x[j] + e * Tp[b * kTile + j];
+                x[j] = (4 * j > b || p > pb) ? v : x[j];
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
     };
     for_each_index(column, std::make_integer_sequence<int, kTile>());
 }
