@@ -76,26 +76,49 @@ __global__ __launch_bounds__(256) void diag_kernel(const double* __restrict__ H,
 }
 
 // perm[rank(i)] = i, rank = number of columns with a larger diagonal, or an equal one and a
-// smaller index (a stable descending order).
+// smaller index (a stable descending order).  64 columns i per workgroup; each wave counts over
+// a quarter of every 1024-value chunk of the diagonal staged in LDS (one value per step, read
+// by the wave's lanes alike), and the four counts are added.
 __global__ __launch_bounds__(256) void order_kernel(const double* __restrict__ diag, int64_t n,
                                                     int* __restrict__ perm) {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (i >= n) return;
-    const double d = diag[i];
-    int64_t rank = 0;
-    for (int64_t j = 0; j < n; ++j) {
-        const double e = diag[j];
-        rank += (e > d || (e == d && j < i)) ? 1 : 0;
+    __shared__ double chunk[1024];
+    __shared__ int part_rank[4][64];
+    const int il = threadIdx.x & 63, part = threadIdx.x >> 6;
+    const int64_t i = (int64_t)blockIdx.x * 64 + il;
+    const double d = i < n ? diag[i] : 0.0;
+    int rank = 0;
+    for (int64_t c0 = 0; c0 < n; c0 += 1024) {
+        __syncthreads();                                          // the previous chunk is used
+        for (int t = threadIdx.x; t < 1024; t += 256) chunk[t] = c0 + t < n ? diag[c0 + t] : 0.0;
+        __syncthreads();
+        const int64_t jb = c0 + part * 256;
+        const int m = (int)(n - jb < 256 ? (n - jb > 0 ? n - jb : 0) : 256);
+        for (int jj = 0; jj < m; ++jj) {
+            const double e = chunk[part * 256 + jj];
+            rank += (e > d || (e == d && jb + jj < i)) ? 1 : 0;
+        }
     }
-    perm[rank] = (int)i;
+    part_rank[part][il] = rank;
+    __syncthreads();
+    if (part == 0 && i < n) perm[part_rank[0][il] + part_rank[1][il] + part_rank[2][il] + part_rank[3][il]] = (int)i;
 }
 
-// lambda = damp * (sum of the diagonal in index order) / n, one lane.
-__global__ void damping_kernel(const double* __restrict__ diag, int64_t n, double damp,
-                               double* __restrict__ lambda) {
+// lambda = damp * (sum of the diagonal in index order) / n: one wave stages the diagonal in
+// chunks, one lane adds.
+__global__ __launch_bounds__(64) void damping_kernel(const double* __restrict__ diag, int64_t n, double damp,
+                                                     double* __restrict__ lambda) {
+    __shared__ double buf[1024];
     double tr = 0.0;
-    for (int64_t c = 0; c < n; ++c) tr += diag[c];
-    lambda[0] = damp * (tr / (double)n);
+    for (int64_t c0 = 0; c0 < n; c0 += 1024) {
+        __syncthreads();
+        for (int t = threadIdx.x; t < 1024; t += 64) buf[t] = c0 + t < n ? diag[c0 + t] : 0.0;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            const int m = (int)(n - c0 < 1024 ? n - c0 : 1024);
+            for (int k = 0; k < m; ++k) tr += buf[k];
+        }
+    }
+    if (threadIdx.x == 0) lambda[0] = damp * (tr / (double)n);
 }
 
 // ---- factor: blocked, from the last 64-column block backwards ---------------------------
@@ -259,64 +282,72 @@ __global__ __launch_bounds__(4 * kTile) void factor_panel_kernel(double* __restr
     for_each_index(step, std::make_integer_sequence<int, kTile>());
 }
 
-// A_ij -= sum over the block's k, downwards, of (U_ik U_jk) D_k for i <= j < k0: one 64 x 64
-// tile (bi, bj) of the upper triangle per workgroup (tiles below it exit), 4 x 4 values per
-// lane; the block's 64 k in two halves of 32 (the upper first), so that four workgroups fit a
-// CU's LDS: four waves per SIMD to issue the binary64 chains.
+// A_ij -= sum over the block's k, downwards, of (U_ik U_jk) D_k for i <= j < k0: one
+// 16R x 16R tile of the upper triangle (rows i0.., columns j0..) per workgroup (tiles wholly
+// below it exit), R x R values per lane; the block's 64 k in two halves of 32 (the upper
+// first), so that four workgroups of the 64 x 64 tiles fit a CU's LDS: four waves per SIMD to
+// issue the binary64 chains.  The 32 x 32 tiles (R = 2) serve the column of tiles the next
+// block needs, which is on the critical path: four times the workgroups, a quarter of the
+// chain per lane.
 constexpr int kHalf = kTile / 2;
-struct FTrailLds {
-    double Ui[kTile][kHalf + 1];   // Ui[ii][kk] = U_{i0+ii, k0+h+kk}
-    double Uj[kTile][kHalf + 1];
+template <int R>
+struct FTrailLdsT {
+    double Ui[16 * R][kHalf + 1];  // Ui[ii][kk] = U_{i0+ii, k0+h+kk}
+    double Uj[16 * R][kHalf + 1];
     double Dk[kTile];
 };
+using FTrailLds = FTrailLdsT<4>;
 
+template <int R>
 __device__ __forceinline__ void factor_trailing_body(double* __restrict__ Uc, const double* __restrict__ D,
-                                                     int64_t n, int64_t k0, int64_t bi, int64_t bj,
-                                                     FTrailLds& L) {
-    if (bi > bj) return;
-    const int64_t i0 = bi * kTile, j0 = bj * kTile;
+                                                     int64_t n, int64_t k0, int64_t i0, int64_t j0,
+                                                     FTrailLdsT<R>& L) {
+    constexpr int B = 16 * R;
+    if (i0 > j0 + B - 1) return;
     if (threadIdx.x < kTile) L.Dk[threadIdx.x] = D[k0 + threadIdx.x];
     const int tr = threadIdx.x / 16, tc = threadIdx.x % 16;
-    double acc[4][4];
+    double acc[R][R];
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int a = 0; a < R; ++a)
 #pragma unroll
-        for (int b = 0; b < 4; ++b) acc[a][b] = Uc[(j0 + tc + 16 * b) * n + i0 + tr + 16 * a];
+        for (int b = 0; b < R; ++b) acc[a][b] = Uc[(j0 + tc + 16 * b) * n + i0 + tr + 16 * a];
     for (int h = kHalf; h >= 0; h -= kHalf) {
         __syncthreads();                                          // the previous half is used
-        for (int t = threadIdx.x; t < kTile * kHalf; t += 256) {
-            const int kk = t / kTile, r = t % kTile;              // coalesced over r
+        for (int t = threadIdx.x; t < B * kHalf; t += 256) {
+            const int kk = t / B, r = t % B;                      // coalesced over r
             L.Ui[r][kk] = Uc[(k0 + h + kk) * n + i0 + r];
             L.Uj[r][kk] = Uc[(k0 + h + kk) * n + j0 + r];
         }
         __syncthreads();
+#pragma unroll(R == 2 ? 4 : 2)
         for (int kk = kHalf - 1; kk >= 0; --kk) {
-            double ua[4], ub[4];
+            double ua[R], ub[R];
 #pragma unroll
-            for (int a = 0; a < 4; ++a) ua[a] = L.Ui[tr + 16 * a][kk];
+            for (int a = 0; a < R; ++a) ua[a] = L.Ui[tr + 16 * a][kk];
 #pragma unroll
-            for (int b = 0; b < 4; ++b) ub[b] = L.Uj[tc + 16 * b][kk];
+            for (int b = 0; b < R; ++b) ub[b] = L.Uj[tc + 16 * b][kk];
             const double dk = L.Dk[h + kk];
 #pragma unroll
-            for (int a = 0; a < 4; ++a)
+            for (int a = 0; a < R; ++a)
 #pragma unroll
-                for (int b = 0; b < 4; ++b) acc[a][b] = acc[a][b] - (ua[a] * ub[b]) * dk;
+                for (int b = 0; b < R; ++b) acc[a][b] = acc[a][b] - (ua[a] * ub[b]) * dk;
         }
     }
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int a = 0; a < R; ++a)
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
+        for (int b = 0; b < R; ++b) {
             const int64_t i = i0 + tr + 16 * a, j = j0 + tc + 16 * b;
             if (i <= j) Uc[j * n + i] = acc[a][b];
         }
 }
 
-// Tiles (bi, bj0 + blockIdx.x), bi = blockIdx.y.
+// Tiles (blockIdx.y, blockIdx.x) of 16R x 16R in the columns from j0.
+template <int R>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void factor_trailing_kernel(
-        double* __restrict__ Uc, const double* __restrict__ D, int64_t n, int64_t k0, int64_t bj0) {
-    __shared__ FTrailLds L;
-    factor_trailing_body(Uc, D, n, k0, blockIdx.y, bj0 + blockIdx.x, L);
+        double* __restrict__ Uc, const double* __restrict__ D, int64_t n, int64_t k0, int64_t j0) {
+    __shared__ FTrailLdsT<R> L;
+    factor_trailing_body<R>(Uc, D, n, k0, (int64_t)blockIdx.y * 16 * R, j0 + (int64_t)blockIdx.x * 16 * R, L);
 }
 
 // Look-ahead: the next diagonal block [kd, kd + 64) (workgroup 0, once the column of tiles it
@@ -333,7 +364,7 @@ __global__ __launch_bounds__(256) void factor_lookahead_kernel(
         factor_diag_body(Uc, D, n, kd, status, L.d);
     } else {
         const int64_t idx = blockIdx.x - 1;
-        factor_trailing_body(Uc, D, n, k0, idx / nb, idx % nb, L.t);
+        factor_trailing_body<4>(Uc, D, n, k0, idx / nb * kTile, idx % nb * kTile, L.t);
     }
 }
 
@@ -452,64 +483,71 @@ __global__ __launch_bounds__(4 * kTile) void tile_kernel(const In* __restrict__ 
 }
 
 // X[r][k] += sum over the tile's b (in order) of Et[r][b] * U_{a0+b, k}, for k in [kstart,
-// kend): one 64 x 64 output block (column block bx, row block by) per workgroup, 4 x 4 values
-// per lane, the terms staged 32 at a time (so that four workgroups fit a CU's LDS: four waves
-// per SIMD to issue the binary64 chains).
-struct QTrailLds {
-    double Es[kTile][kHalf + 1];   // Es[row][b]
-    double Us[kHalf][kTile + 1];   // Us[b][col]
+// kend): one 16R x 16R output block (column block bx, row block by) per workgroup, R x R values
+// per lane, the terms staged 32 at a time (so that four workgroups of the 64 x 64 blocks fit a
+// CU's LDS: four waves per SIMD to issue the binary64 chains).  The 32 x 32 blocks (R = 2)
+// serve the next tile's columns, which are on the critical path.
+template <int R>
+struct QTrailLdsT {
+    double Es[16 * R][kHalf + 1];  // Es[row][b]
+    double Us[kHalf][16 * R + 1];  // Us[b][col]
 };
+using QTrailLds = QTrailLdsT<4>;
 
+template <int R>
 __device__ __forceinline__ void trailing_body(const double* __restrict__ Et, const double* __restrict__ Uc,
                                               int64_t rows, int64_t n, int64_t a0, int64_t kstart,
                                               int64_t kend, double* __restrict__ X, int64_t bx,
-                                              int64_t by, QTrailLds& L) {
-    const int64_t r0 = by * kTile;
-    const int64_t k0 = kstart + bx * kTile;
-    const int tr = threadIdx.x / 16, tc = threadIdx.x % 16;      // 16 x 16 lanes, 4 x 4 each
-    double acc[4][4];
+                                              int64_t by, QTrailLdsT<R>& L) {
+    constexpr int B = 16 * R;
+    const int64_t r0 = by * B;
+    const int64_t k0 = kstart + bx * B;
+    const int tr = threadIdx.x / 16, tc = threadIdx.x % 16;      // 16 x 16 lanes, R x R each
+    double acc[R][R];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < R; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < R; ++j) {
             const int64_t r = r0 + tr + 16 * i, k = k0 + tc + 16 * j;
             acc[i][j] = (r < rows && k < kend) ? X[r * n + k] : 0.0;
         }
     for (int h = 0; h < kTile; h += kHalf) {
         __syncthreads();                                          // the previous half is used
-        for (int t = threadIdx.x; t < kTile * kHalf; t += 256) {
+        for (int t = threadIdx.x; t < B * kHalf; t += 256) {
             const int rr = t / kHalf, b = t % kHalf;              // coalesced over b
             L.Es[rr][b] = r0 + rr < rows ? Et[(r0 + rr) * kTile + h + b] : 0.0;
             const int cc = t / kHalf, bb = t % kHalf;
             L.Us[bb][cc] = k0 + cc < kend ? Uc[(k0 + cc) * n + a0 + h + bb] : 0.0;
         }
         __syncthreads();
+#pragma unroll(R == 2 ? 4 : 2)
         for (int b = 0; b < kHalf; ++b) {
-            double e[4], u[4];
+            double e[R], u[R];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) e[i] = L.Es[tr + 16 * i][b];
+            for (int i = 0; i < R; ++i) e[i] = L.Es[tr + 16 * i][b];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) u[j] = L.Us[b][tc + 16 * j];
+            for (int j = 0; j < R; ++j) u[j] = L.Us[b][tc + 16 * j];
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < R; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = acc[i][j] + e[i] * u[j];
+                for (int j = 0; j < R; ++j) acc[i][j] = acc[i][j] + e[i] * u[j];
         }
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < R; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < R; ++j) {
             const int64_t r = r0 + tr + 16 * i, k = k0 + tc + 16 * j;
             if (r < rows && k < kend) X[r * n + k] = acc[i][j];
         }
 }
 
+template <int R>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void trailing_kernel(
         const double* __restrict__ Et, const double* __restrict__ Uc, int64_t rows, int64_t n, int64_t a0,
         int64_t kstart, int64_t kend, double* __restrict__ X) {
-    __shared__ QTrailLds L;
-    trailing_body(Et, Uc, rows, n, a0, kstart, kend, X, blockIdx.x, blockIdx.y, L);
+    __shared__ QTrailLdsT<R> L;
+    trailing_body<R>(Et, Uc, rows, n, a0, kstart, kend, X, blockIdx.x, blockIdx.y, L);
 }
 
 // Look-ahead: the next tile (workgroups 0 .. ntile-1, its errors into Etn) beside the rest of
@@ -532,7 +570,7 @@ __global__ __launch_bounds__(4 * kTile) __attribute__((amdgpu_waves_per_eu(3))) 
                       L.t);
     } else {
         const int64_t idx = blockIdx.x - ntile;
-        trailing_body(Etc, Uc, rows, n, a0c, kstart, n, X, idx % ncb, idx / ncb, L.q);
+        trailing_body<4>(Etc, Uc, rows, n, a0c, kstart, n, X, idx % ncb, idx / ncb, L.q);
     }
 }
 
@@ -586,8 +624,8 @@ int run_ldlq(const void* wv, int64_t rows, int64_t n, int block, const double* H
 
     hipLaunchKernelGGL(clear_status_kernel, dim3(1), dim3(1), 0, st, status);
     hipLaunchKernelGGL(diag_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, H, n, diag);
-    hipLaunchKernelGGL(order_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, diag, n, perm);
-    hipLaunchKernelGGL(damping_kernel, dim3(1), dim3(1), 0, st, diag, n, damp, lambda);
+    hipLaunchKernelGGL(order_kernel, dim3(blocks_for(n, 64)), dim3(256), 0, st, diag, n, perm);
+    hipLaunchKernelGGL(damping_kernel, dim3(1), dim3(64), 0, st, diag, n, damp, lambda);
     if (hipGetLastError() != hipSuccess) return NVFP4_ERR_HIP;
     hipLaunchKernelGGL(init_a_kernel, dim3(blocks_for(n * n, 256)), dim3(256), 0, st, H, perm, lambda,
                        n, Uc);
@@ -599,8 +637,8 @@ int run_ldlq(const void* wv, int64_t rows, int64_t n, int block, const double* H
         hipLaunchKernelGGL(factor_panel_kernel, dim3(blocks_for(k0, kTile)), dim3(4 * kTile), 0, st, Uc, D,
                            n, k0);
         const int64_t nb = k0 / kTile - 1;                         // the next block's tile column
-        hipLaunchKernelGGL(factor_trailing_kernel, dim3(1, (unsigned)(nb + 1)), dim3(256), 0, st, Uc, D, n,
-                           k0, nb);
+        hipLaunchKernelGGL(factor_trailing_kernel<2>, dim3(2, (unsigned)(2 * (nb + 1))), dim3(256), 0, st, Uc,
+                           D, n, k0, nb * kTile);
         hipLaunchKernelGGL(factor_lookahead_kernel, dim3((unsigned)(1 + nb * nb)), dim3(256), 0, st, Uc, D,
                            n, k0, nb > 0 ? nb : 1, k0 - kTile, status);
         if (hipGetLastError() != hipSuccess) return NVFP4_ERR_HIP;
@@ -616,8 +654,8 @@ int run_ldlq(const void* wv, int64_t rows, int64_t n, int block, const double* H
     for (int64_t a0 = 0; a0 + kTile < n; a0 += kTile) {
         double* Etc = Et + ((a0 / kTile) & 1) * rows * kTile;
         double* Etn = Et + (((a0 / kTile) + 1) & 1) * rows * kTile;
-        hipLaunchKernelGGL(trailing_kernel, dim3(1, rblocks), dim3(256), 0, st, Etc, Uc, rows, n, a0,
-                           a0 + kTile, a0 + 2 * kTile, X);
+        hipLaunchKernelGGL(trailing_kernel<2>, dim3(2, blocks_for(rows, 32)), dim3(256), 0, st, Etc, Uc, rows,
+                           n, a0, a0 + kTile, a0 + 2 * kTile, X);
         const int64_t rest = n - (a0 + 2 * kTile);                  // columns past the next tile
         const int64_t ncb = (rest + kTile - 1) / kTile;
         hipLaunchKernelGGL(tile_lookahead_kernel<In>, dim3((unsigned)(rblocks + ncb * rblocks)),
