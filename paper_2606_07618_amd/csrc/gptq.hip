@@ -59,6 +59,11 @@ __device__ __forceinline__ void for_each_index(F&& f, std::integer_sequence<int,
 
 // Lane l of a quad broadcasts v to the quad's four lanes (a DPP quad permutation).
 template <int L>
+__device__ __forceinline__ uint32_t quad_bcast_u32(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, L * 0x55, 0xF, 0xF, false);
+}
+
+template <int L>
 __device__ __forceinline__ double quad_bcast(double v) {
     constexpr int ctrl = L * 0x55;                    // quad_perm(L, L, L, L)
     const uint64_t b = (uint64_t)__double_as_longlong(v);
@@ -381,18 +386,16 @@ __global__ __launch_bounds__(256) void init_x_kernel(const In* __restrict__ w, c
 
 // One tile of 64 columns, right-looking, four lanes (a quad) per row and 64 rows per
 // workgroup: lane p of a quad holds the running values of tile columns 4j + p, j = 0..15, in
-// registers.  Column b's value is broadcast to the quad, which quantizes it (every lane the
-// same operations, so the same error), and each lane then adds error_b * U_b,a to each of its
-// columns a > b.  Every value thus receives its terms b = a0, a0 + 1, ... in ascending order,
-// as the sequential definition adds them.  The row's weights and scale bytes are staged in LDS
-// (read by the four lanes alike), U's tile block too, each lane's columns of a U row
-// contiguous.  A column's work holds no branch: its scale, weight, midpoint products and U
-// values do not depend on the running value, so they are read and formed ahead of the chain
-// value -> quotient -> E2M1 index -> error -> the next column's value that bounds the walk.
+// registers, with their weights and scale codes.  Column b's value is broadcast to the quad,
+// which quantizes it (every lane the same operations, so the same error), and each lane then
+// adds error_b * U_b,a to each of its columns a > b.  Every value thus receives its terms
+// b = a0, a0 + 1, ... in ascending order, as the sequential definition adds them.  U's tile
+// block is staged in LDS, each lane's columns of a U row contiguous.  A column's work holds
+// no branch: its scale, weight, midpoint products and U values do not depend on the running
+// value, so they are formed ahead of the chain value -> quotient -> E2M1 index -> error -> the
+// next column's value that bounds the walk.
 struct alignas(16) TileLds {
     double T[kTile][kTile];        // T[b][16 p + j] = U_{a0+b, a0+4j+p}
-    float wsv[kTile][kTile + 1];   // wsv[rr][a]: the weight of tile column a, row rr
-    uint8_t scs[kTile][kTile];     // scs[rr][a]: its block's scale code
     int pc[kTile];
 };
 
@@ -414,18 +417,16 @@ __device__ __forceinline__ void tile_body(const In* __restrict__ w, const int* _
     const int64_t r = rblock * kTile + rr;
     if (r >= rows) return;                   // whole quads: the broadcasts stay inside live rows
     const int64_t nb = n / block;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {           // this lane's share of the row's weights and scales
-        const int a = 16 * p + j, c = L.pc[a];
-        L.wsv[rr][a] = load_w<In>(w, r * n + c);
-        L.scs[rr][a] = scales[r * nb + c / block];
-    }
     double x[16];
+    float wr[16];                            // weights of this lane's columns
+    uint32_t sc4[4] = {0u, 0u, 0u, 0u};      // their scale codes, four to a register
 #pragma unroll
-    for (int j = 0; j < 16; ++j) x[j] = X[r * n + a0 + 4 * j + p];
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");   // the quad's LDS stores, then reads
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    for (int j = 0; j < 16; ++j) {
+        const int c = L.pc[4 * j + p];
+        x[j] = X[r * n + a0 + 4 * j + p];
+        wr[j] = load_w<In>(w, r * n + c);
+        sc4[j >> 2] |= (uint32_t)scales[r * nb + c / block] << (8 * (j & 3));
+    }
     const float S = tensor_scale[0];
     const double halfS = 0.5 * (double)S;
     const double* Tp = &L.T[0][16 * p];
@@ -434,9 +435,9 @@ __device__ __forceinline__ void tile_body(const In* __restrict__ w, const int* _
     auto column = [&](auto bc) {
         constexpr int b = decltype(bc)::value, pb = b & 3, jb = b >> 2;
         // independent of the running values
-        const int code = L.scs[rr][b];
+        const int code = (int)((quad_bcast_u32<pb>(sc4[jb >> 2]) >> (8 * (jb & 3))) & 0xFFu);
         const double s = e4m3_f64(code);
-        const double wv = (double)L.wsv[rr][b];
+        const double wv = (double)__uint_as_float(quad_bcast_u32<pb>(__float_as_uint(wr[jb])));
         const double gscale = s * halfS;     // E2M1(k) s S = (2 E2M1(k)) (s S / 2), all exact
         double m[7];                          // the midpoints times s (exact: <= 7 significant bits)
 #pragma unroll
@@ -555,7 +556,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void t
 // (the other workgroups, ncb column blocks per row block).  The next tile's columns already
 // hold every earlier term; the two touch disjoint values.
 template <typename In>
-__global__ __launch_bounds__(4 * kTile) __attribute__((amdgpu_waves_per_eu(3))) void tile_lookahead_kernel(
+__global__ __launch_bounds__(4 * kTile) __attribute__((amdgpu_waves_per_eu(4))) void tile_lookahead_kernel(
         const In* __restrict__ w, const int* __restrict__ perm, const double* __restrict__ Uc,
         const uint8_t* __restrict__ scales, const float* __restrict__ tensor_scale, int64_t rows,
         int64_t n, int block, int64_t a0n, double* __restrict__ X, double* __restrict__ Etn,
