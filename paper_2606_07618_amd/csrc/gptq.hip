@@ -7,21 +7,24 @@
 // upper triangular).  LDLQ and GPTQ give the same result.  Everything is binary64 with a
 // fixed order of correctly rounded operations per value:
 //   * factor: Hp is factored in place (column-major) in 64-column blocks from the last: the
-//     block's own columns in LDS, right-looking from its last column (each column's updates
-//     to the block's remaining triangle in parallel); then the rows above it, each a 64-column
-//     triangular solve, also right-looking; then the block's contribution (U_ik U_jk) D_k, k
-//     walked downwards, is subtracted from the rest of the upper triangle in 64 x 64 tiles,
-//     first the column of tiles the next block needs, then the rest beside the next block's
-//     own factor (look-ahead).  So each element receives its terms k = n-1, ..., j+1 in that
-//     order.
+//     block's own columns right-looking from its last column (rows in registers, each
+//     column's updates to the block's remaining triangle in parallel); then the rows above
+//     it, each a 64-column triangular solve, also right-looking; then the block's
+//     contribution (U_ik U_jk) D_k, k walked downwards, is subtracted from the rest of the
+//     upper triangle in tiles, first the column of tiles the next block needs, then the rest
+//     beside the next block's own factor (look-ahead).  So each element receives its terms
+//     k = n-1, ..., j+1 in that order.
 //   * quantize: columns are taken in tiles of 64.  A tile kernel gives each row a quad of
 //     lanes holding the tile's running values in registers: column b's value is quantized and
 //     its error times U added to the tile's later columns, b = a0, a0 + 1, ... in order.  A
 //     trailing-update kernel then adds the tile's 64 errors times U to every later column,
-//     term by term in tile order, in 64 x 64 output blocks with 4 x 4 values per lane: first
-//     to the next tile's columns, then to the rest beside the next tile's kernel (look-ahead).
-//     Every x_a therefore receives its terms b = 0, 1, ... in ascending order, as the
-//     sequential definition adds them.
+//     term by term in tile order: first to the next tile's columns, then to the rest beside
+//     the next tile's kernel (look-ahead).  Every x_a therefore receives its terms
+//     b = 0, 1, ... in ascending order, as the sequential definition adds them.
+//   The sequential kernels (diagonal block, panel, tile) hold no branch per step: the columns
+//   are interleaved over a quad's lanes (column 4m + q in lane q), so a step's updates need at
+//   most one select, and its operands that do not depend on the running values are formed
+//   ahead of the dependent chain.
 // Q(x) is the quantizers' rounding: y = RN32(RN32(x) / S), nibble sign(y) << 3 | RNE_FP4(|y| /
 // s), w^ = +-E2M1 * s * S (exact in binary64).
 #include <hip/hip_runtime.h>
