@@ -319,14 +319,32 @@ __device__ __forceinline__ void factor_trailing_body(double* __restrict__ Uc, co
     for (int a = 0; a < R; ++a)
 #pragma unroll
         for (int b = 0; b < R; ++b) acc[a][b] = Uc[(j0 + tc + 16 * b) * n + i0 + tr + 16 * a];
+    // each half's operands are loaded into registers while the previous half is computed
+    constexpr int kPer = B * kHalf / 256;
+    double pi[kPer], pj[kPer];
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) {
+        const int t = threadIdx.x + 256 * e, kk = t / B, r = t % B;      // coalesced over r
+        pi[e] = Uc[(k0 + kHalf + kk) * n + i0 + r];
+        pj[e] = Uc[(k0 + kHalf + kk) * n + j0 + r];
+    }
     for (int h = kHalf; h >= 0; h -= kHalf) {
         __syncthreads();                                          // the previous half is used
-        for (int t = threadIdx.x; t < B * kHalf; t += 256) {
-            const int kk = t / B, r = t % B;                      // coalesced over r
-            L.Ui[r][kk] = Uc[(k0 + h + kk) * n + i0 + r];
-            L.Uj[r][kk] = Uc[(k0 + h + kk) * n + j0 + r];
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            const int t = threadIdx.x + 256 * e, kk = t / B, r = t % B;
+            L.Ui[r][kk] = pi[e];
+            L.Uj[r][kk] = pj[e];
         }
         __syncthreads();
+        if (h > 0) {
+#pragma unroll
+            for (int e = 0; e < kPer; ++e) {
+                const int t = threadIdx.x + 256 * e, kk = t / B, r = t % B;
+                pi[e] = Uc[(k0 + kk) * n + i0 + r];
+                pj[e] = Uc[(k0 + kk) * n + j0 + r];
+            }
+        }
 #pragma unroll(R == 2 ? 4 : 2)
         for (int kk = kHalf - 1; kk >= 0; --kk) {
             double ua[R], ub[R];
@@ -398,7 +416,8 @@ __global__ __launch_bounds__(256) void init_x_kernel(const In* __restrict__ w, c
 // value, so they are formed ahead of the chain value -> quotient -> E2M1 index -> error -> the
 // next column's value that bounds the walk.
 struct alignas(16) TileLds {
-    double T[kTile][kTile];        // T[b][16 p + j] = U_{a0+b, a0+4j+p}
+    double T[kTile][kTile + 2];    // T[b][16 p + j] = U_{a0+b, a0+4j+p} (rows padded: the staging
+                                   // writes of a wave, one per row, spread over the banks)
     int pc[kTile];
 };
 
@@ -433,6 +452,7 @@ __device__ __forceinline__ void tile_body(const In* __restrict__ w, const int* _
     const float S = tensor_scale[0];
     const double halfS = 0.5 * (double)S;
     const double* Tp = &L.T[0][16 * p];
+    constexpr int kTRow = kTile + 2;
     uint8_t* crow = codes + r * n;
     double* erow = Et + r * kTile;
     auto column = [&](auto bc) {
@@ -464,7 +484,7 @@ __device__ __forceinline__ void tile_body(const In* __restrict__ w, const int* _
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
             if (4 * j + 3 > b) {             // some lane of the quad holds a column past b
-                const double v = x[j] + e * Tp[b * kTile + j];
+                const double v = x[j] + e * Tp[b * kTRow + j];
                 x[j] = (4 * j > b || p > pb) ? v : x[j];
             }
         }
@@ -515,15 +535,28 @@ __device__ __forceinline__ void trailing_body(const double* __restrict__ Et, con
             const int64_t r = r0 + tr + 16 * i, k = k0 + tc + 16 * j;
             acc[i][j] = (r < rows && k < kend) ? X[r * n + k] : 0.0;
         }
+    // each half's operands are loaded into registers while the previous half is computed
+    constexpr int kPer = B * kHalf / 256;
+    double pe[kPer], pu[kPer];
+    auto fetch = [&](int h) {
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            const int t = threadIdx.x + 256 * e, rr = t / kHalf, b = t % kHalf;   // coalesced over b
+            pe[e] = r0 + rr < rows ? Et[(r0 + rr) * kTile + h + b] : 0.0;
+            pu[e] = k0 + rr < kend ? Uc[(k0 + rr) * n + a0 + h + b] : 0.0;
+        }
+    };
+    fetch(0);
     for (int h = 0; h < kTile; h += kHalf) {
         __syncthreads();                                          // the previous half is used
-        for (int t = threadIdx.x; t < B * kHalf; t += 256) {
-            const int rr = t / kHalf, b = t % kHalf;              // coalesced over b
-            L.Es[rr][b] = r0 + rr < rows ? Et[(r0 + rr) * kTile + h + b] : 0.0;
-            const int cc = t / kHalf, bb = t % kHalf;
-            L.Us[bb][cc] = k0 + cc < kend ? Uc[(k0 + cc) * n + a0 + h + bb] : 0.0;
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            const int t = threadIdx.x + 256 * e, rr = t / kHalf, b = t % kHalf;
+            L.Es[rr][b] = pe[e];
+            L.Us[b][rr] = pu[e];
         }
         __syncthreads();
+        if (h + kHalf < kTile) fetch(h + kHalf);
 #pragma unroll(R == 2 ? 4 : 2)
         for (int b = 0; b < kHalf; ++b) {
             double e[R], u[R];
