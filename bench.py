@@ -53,12 +53,12 @@ def parse():
                     help="also run a plain device copy of known size (for counter scaling)")
     ap.add_argument("--no-rows", action="store_true",
                     help="skip the window / reference-scale / online / GPTQ measurements")
-    ap.add_argument("--profile-config", choices=("c0", "c2", "c3", "c3w", "c4", "f3"), default=None,
+    ap.add_argument("--profile-config", choices=("c0", "c2", "c3", "c3w", "c4", "f3", "f4"), default=None,
                     help="run only one other configuration's launches (a few of each, for "
                          "rocprofv3 counter runs) and exit: c0 the FP32 1024x1024 matrix, c2 the "
                          "8192x8192 block-size sweep, c3 the online tensors, c4 one "
                          "Llama-3-70B-shaped layer, f3 the fused SwiGLU quantizer and its "
-                         "unfused pair")
+                         "unfused pair, f4 GPTQ on q_proj")
     ap.add_argument("--c4-layers", type=int, default=80,
                     help="Llama-3-70B-shaped layers to stream through the WMSE quantizer "
                          "(80, the default, is the whole model)")
@@ -298,18 +298,25 @@ def measure_rows(nv, workloads, torch, dev, layer):
     out["f3_fused_swiglu"] = measure_fused_swiglu(nv, workloads, torch, dev)
 
     # GPTQ (LDLQ) with ScaleSweep-WMSE scales fixed beforehand, q_proj and a synthetic Hessian
-    g = workloads.generator(dev, 61, 99)
-    X = torch.randn((1024, 4096), generator=g, device=dev, dtype=torch.float64) * \
-        torch.exp(0.7 * torch.randn(4096, generator=g, device=dev, dtype=torch.float64))
-    H = (X.T @ X).contiguous()
-    del X
-    imp = torch.diagonal(H).float().contiguous()
-    _, scg, Sg = nv.quantize(xq, "scalesweep_wmse", 16, weight=imp)
+    H, scg, Sg = gptq_inputs(nv, workloads, torch, dev, xq)
     ms_gptq = _timed(torch, lambda: nv.ldlq(xq, H, scg, Sg, 16, 0.01, check=False), 3)
     out["f4_gptq"] = {"workload": "q_proj [4096, 4096] bf16, Hessian X^T X of 1024 synthetic "
                                   "tokens, ScaleSweep-WMSE scales, damping 0.01",
                       "ms_per_call": round(ms_gptq, 2)}
     return out
+
+
+def gptq_inputs(nv, workloads, torch, dev, xq):
+    """A synthetic Hessian X^T X of 1024 tokens (columns of log-normal scale) for the weight xq,
+    and xq's ScaleSweep-WMSE scales with the Hessian diagonal as importance."""
+    g = workloads.generator(dev, 61, 99)
+    X = torch.randn((1024, xq.shape[1]), generator=g, device=dev, dtype=torch.float64) * \
+        torch.exp(0.7 * torch.randn(xq.shape[1], generator=g, device=dev, dtype=torch.float64))
+    H = (X.T @ X).contiguous()
+    del X
+    imp = torch.diagonal(H).float().contiguous()
+    _, scg, Sg = nv.quantize(xq, "scalesweep_wmse", 16, weight=imp)
+    return H, scg, Sg
 
 
 def measure_llama70b(nv, workloads, torch, dev, layers):
@@ -416,6 +423,11 @@ def profile_config(name, nv, workloads, torch, dev, copy_calibration):
             wt = imp if m == "scalesweep_wmse" else None
             run(f"f3 fused {m}", lambda: nv.quantize_online_swiglu(gate, up, m, 0.004, wt, layout="swizzled"))
             run(f"f3 unfused quantizer {m}", lambda: nv.quantize_online(h, m, 0.004, 16, wt, layout="swizzled"))
+    elif name == "f4":
+        xq = workloads.llama8b_layer(dev)["q_proj"][0]
+        H, scg, Sg = gptq_inputs(nv, workloads, torch, dev, xq)
+        run("f4 GPTQ q_proj [4096, 4096] bf16, ScaleSweep-WMSE scales, damping 0.01",
+            lambda: nv.ldlq(xq, H, scg, Sg, 16, 0.01, check=False))
     else:
         lay = workloads.llama70b_layer(0, dev)
         xs = [lay[n][0] for n in lay]

@@ -171,6 +171,9 @@ __device__ __forceinline__ void factor_diag_body(double* __restrict__ Uc, double
     double v[16];                            // A (then U) of (k0 + i, k0 + 4m + q)
 #pragma unroll
     for (int m = 0; m < 16; ++m) v[m] = Uc[(k0 + 4 * m + q) * n + k0 + i];
+    // the column buffers start at zero: a step reads slots of rows it does not update (their
+    // results are discarded by the selects)
+    if (tid < 2 * kTile) L.col[tid / kTile][tid % kTile] = 0.0;
     // column 63: its diagonal, then its U, and A_62,62 for step 63
     if (i == kTile - 1 && q == 3) L.Db[kTile - 1] = v[15];
     __syncthreads();
