@@ -194,7 +194,9 @@ __device__ __forceinline__ void factor_diag_body(double* __restrict__ Uc, double
         const double ui = c[quad_slot(i)];
         const double* cq = c + 16 * q;
         // the updates of this step: A_ij, i <= j = 4m + q < kk, in two halves of eight columns
-        // (U values read together first; each new value formed in every lane, then selected)
+        // (U values read together first).  Values left of the diagonal (j < i) are updated too:
+        // they feed nothing (no diagonal, division, published value or store reads them), so
+        // only the column bound j < kk needs a select, in one register per step.
 #pragma unroll
         for (int h = 0; h < 16; h += 8) {
             double uj[8];
@@ -202,11 +204,11 @@ __device__ __forceinline__ void factor_diag_body(double* __restrict__ Uc, double
             for (int m = 0; m < 8; ++m) uj[m] = 4 * (h + m) < kk ? cq[h + m] : 0.0;
 #pragma unroll
             for (int m = 0; m < 8; ++m) {
-                if (4 * (h + m) < kk) {
-                    double nv = v[h + m] - (ui * uj[m]) * d;
+                const int mm = h + m;
+                if (4 * mm < kk) {
+                    double nv = v[mm] - (ui * uj[m]) * d;
                     asm volatile("" : "+v"(nv));
-                    const int j = 4 * (h + m) + q;
-                    v[h + m] = (j >= i && j < kk) ? nv : v[h + m];
+                    v[mm] = (4 * mm + 3 < kk || q < kk - 4 * mm) ? nv : v[mm];
                 }
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -382,7 +384,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
 // Look-ahead: the next diagonal block [kd, kd + 64) (workgroup 0, once the column of tiles it
 // needs has been updated) beside the rest of the current block's trailing update, tiles with
 // bj < nb (the other workgroups, nb x nb of them).  The two touch disjoint elements.
-__global__ __launch_bounds__(256) void factor_lookahead_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void factor_lookahead_kernel(
         double* __restrict__ Uc, double* __restrict__ D, int64_t n, int64_t k0, int64_t nb, int64_t kd,
         int* __restrict__ status) {
     __shared__ union {
