@@ -517,29 +517,39 @@ __global__ __launch_bounds__(4 * kTile) void tile_kernel(const In* __restrict__ 
 // CU's LDS: four waves per SIMD to issue the binary64 chains).  The 32 x 32 blocks (R = 2)
 // serve the next tile's columns, which are on the critical path.
 template <int R>
-struct QTrailLdsT {
-    double Es[16 * R][kHalf + 1];  // Es[row][b]
-    double Us[kHalf][16 * R + 1];  // Us[b][col]
+struct alignas(16) QTrailLdsT {
+    double Es[kHalf][16 * R + 2];  // Es[b][row] (rows padded: 16-byte rows, staging writes spread)
+    double Us[kHalf][16 * R + 2];  // Us[b][col]
 };
 using QTrailLds = QTrailLdsT<4>;
 
+// Lane (tr, tc) owns rows r0 + R tr .. + R - 1 and columns k0 + R tc .. + R - 1, so that its X
+// values and its operands of a step sit in 16-byte pairs.  kstart, kend and the blocks' columns
+// are multiples of 32, so a lane's columns are all inside [kstart, kend) or all outside.
 template <int R>
 __device__ __forceinline__ void trailing_body(const double* __restrict__ Et, const double* __restrict__ Uc,
                                               int64_t rows, int64_t n, int64_t a0, int64_t kstart,
                                               int64_t kend, double* __restrict__ X, int64_t bx,
                                               int64_t by, QTrailLdsT<R>& L) {
+    static_assert(R % 2 == 0, "pairs of values");
     constexpr int B = 16 * R;
     const int64_t r0 = by * B;
     const int64_t k0 = kstart + bx * B;
     const int tr = threadIdx.x / 16, tc = threadIdx.x % 16;      // 16 x 16 lanes, R x R each
+    const int64_t kc = k0 + R * tc;
+    const bool cols_in = kc < kend;
     double acc[R][R];
 #pragma unroll
-    for (int i = 0; i < R; ++i)
+    for (int i = 0; i < R; ++i) {
+        const int64_t r = r0 + R * tr + i;
+        const double2* src = reinterpret_cast<const double2*>(X + r * n + kc);
 #pragma unroll
-        for (int j = 0; j < R; ++j) {
-            const int64_t r = r0 + tr + 16 * i, k = k0 + tc + 16 * j;
-            acc[i][j] = (r < rows && k < kend) ? X[r * n + k] : 0.0;
+        for (int j = 0; j < R; j += 2) {
+            const double2 v = (r < rows && cols_in) ? src[j / 2] : make_double2(0.0, 0.0);
+            acc[i][j] = v.x;
+            acc[i][j + 1] = v.y;
         }
+    }
     // each half's operands are loaded into registers while the previous half is computed
     constexpr int kPer = B * kHalf / 256;
     double pe[kPer], pu[kPer];
@@ -557,7 +567,7 @@ __device__ __forceinline__ void trailing_body(const double* __restrict__ Et, con
 #pragma unroll
         for (int e = 0; e < kPer; ++e) {
             const int t = threadIdx.x + 256 * e, rr = t / kHalf, b = t % kHalf;
-            L.Es[rr][b] = pe[e];
+            L.Es[b][rr] = pe[e];
             L.Us[b][rr] = pu[e];
         }
         __syncthreads();
@@ -565,10 +575,16 @@ __device__ __forceinline__ void trailing_body(const double* __restrict__ Et, con
 #pragma unroll(R == 2 ? 4 : 2)
         for (int b = 0; b < kHalf; ++b) {
             double e[R], u[R];
+            const double2* ep = reinterpret_cast<const double2*>(&L.Es[b][R * tr]);
+            const double2* up = reinterpret_cast<const double2*>(&L.Us[b][R * tc]);
 #pragma unroll
-            for (int i = 0; i < R; ++i) e[i] = L.Es[tr + 16 * i][b];
-#pragma unroll
-            for (int j = 0; j < R; ++j) u[j] = L.Us[b][tc + 16 * j];
+            for (int i = 0; i < R; i += 2) {
+                const double2 ev = ep[i / 2], uv = up[i / 2];
+                e[i] = ev.x;
+                e[i + 1] = ev.y;
+                u[i] = uv.x;
+                u[i + 1] = uv.y;
+            }
 #pragma unroll
             for (int i = 0; i < R; ++i)
 #pragma unroll
@@ -576,12 +592,14 @@ __device__ __forceinline__ void trailing_body(const double* __restrict__ Et, con
         }
     }
 #pragma unroll
-    for (int i = 0; i < R; ++i)
+    for (int i = 0; i < R; ++i) {
+        const int64_t r = r0 + R * tr + i;
+        if (r < rows && cols_in) {
+            double2* dst = reinterpret_cast<double2*>(X + r * n + kc);
 #pragma unroll
-        for (int j = 0; j < R; ++j) {
-            const int64_t r = r0 + tr + 16 * i, k = k0 + tc + 16 * j;
-            if (r < rows && k < kend) X[r * n + k] = acc[i][j];
+            for (int j = 0; j < R; j += 2) dst[j / 2] = make_double2(acc[i][j], acc[i][j + 1]);
         }
+    }
 }
 
 template <int R>
