@@ -207,7 +207,8 @@ __device__ __forceinline__ void factor_diag_body(double* __restrict__ Uc, double
                 const int mm = h + m;
                 if (4 * mm < kk) {
                     double nv = v[mm] - (ui * uj[m]) * d;
-                    asm volatile("" : "+v"(nv));
+                    asm volatile("" : "+v"(nv));     // formed in every lane, then selected (no
+                                                     // branch around the update and its reads)
                     v[mm] = (4 * mm + 3 < kk || q < kk - 4 * mm) ? nv : v[mm];
                 }
             }
