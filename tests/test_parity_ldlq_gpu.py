@@ -51,6 +51,17 @@ def test_ldlq_parity_small(nv, rows, cols, dtype):
     check(nv, w, H)
 
 
+@pytest.mark.parametrize("rows,cols", [(130, 1024), (7, 1536)])
+def test_ldlq_parity_many_tiles_every_row(nv, rows, cols):
+    """Sixteen and twenty-four 64-column blocks: every look-ahead step of the factor and of the
+    quantization (diagonal block beside the trailing update, tile beside the far columns) runs
+    many times, with ragged row blocks; every row is compared."""
+    g = workloads.generator(DEV, 65, rows, cols)
+    w = workloads.llm_weight(rows, cols, g, DEV, outlier_frac=0.01)
+    H = synthetic_hessian(cols, 2 * cols, rows, spread=0.9)
+    check(nv, w, H)
+
+
 @pytest.mark.parametrize("method,block", [("absmax", 16), ("four_over_six", 32),
                                           ("scalesweep_mse", 64), ("scalesweep_wmse", 128)])
 def test_ldlq_parity_methods_and_blocks(nv, method, block):
