@@ -66,6 +66,16 @@ __device__ __forceinline__ uint32_t quad_bcast_u32(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, L * 0x55, 0xF, 0xF, false);
 }
 
+// Lane l of each 16-lane row broadcasts v to the row's lanes (DPP row_newbcast).
+template <int L>
+__device__ __forceinline__ double row_bcast(double v) {
+    constexpr int ctrl = 0x150 + L;
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, ctrl, 0xF, 0xF, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), ctrl, 0xF, 0xF, false);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
 template <int L>
 __device__ __forceinline__ double quad_bcast(double v) {
     constexpr int ctrl = L * 0x55;                    // quad_perm(L, L, L, L)
@@ -251,45 +261,49 @@ __global__ __launch_bounds__(4 * kTile) void factor_diag_kernel(double* __restri
     factor_diag_body(Uc, D, n, k0, status, L);
 }
 
-// Rows above the block (i < k0), 64 per workgroup, a quad of lanes per row: lane q holds the
-// row's values of block columns 4m + q in registers.  Each row is a triangular solve from the
-// block's last column, right-looking: at step kk the row's value of column kk is final,
-// U_i,kk = A_i,kk / D_kk (broadcast in the quad), and each of the row's columns j < kk loses
-// (U_i,kk U_j,kk) D_kk.  So each value receives its terms kk = 63, 62, ... in the order the
-// column-by-column definition sums them.  A step holds no branch; the block's U and D are
-// staged in LDS (each lane's columns of a U row contiguous).
-__global__ __launch_bounds__(4 * kTile) void factor_panel_kernel(double* __restrict__ Uc,
-                                                                 const double* __restrict__ D, int64_t n,
-                                                                 int64_t k0) {
-    __shared__ double Ub[kTile][kTile];       // Ub[kk][16 q + m] = U_{k0+4m+q, k0+kk}
+// Rows above the block (i < k0), 16 per workgroup, a 16-lane row of lanes per matrix row: lane
+// q holds the row's values of block columns 16m + q (m = 0..3) in registers.  Each row is a
+// triangular solve from the block's last column, right-looking: at step kk the row's value of
+// column kk is final, U_i,kk = A_i,kk / D_kk (broadcast in the lane row), and each of the
+// row's columns j < kk loses (U_i,kk U_j,kk) D_kk.  So each value receives its terms kk = 63,
+// 62, ... in the order the column-by-column definition sums them.  A step holds no branch and
+// at most four updates per lane; the block's U and D are staged in LDS (each lane's columns of
+// a U row contiguous).
+constexpr int kPanelRows = 16;
+__device__ __forceinline__ int row16_slot(int j) { return 4 * (j & 15) + (j >> 4); }
+
+__global__ __launch_bounds__(256) void factor_panel_kernel(double* __restrict__ Uc,
+                                                           const double* __restrict__ D, int64_t n,
+                                                           int64_t k0) {
+    __shared__ double Ub[kTile][kTile];       // Ub[kk][4 q + m] = U_{k0+16m+q, k0+kk}
     __shared__ double Db[kTile];
     const int tid = threadIdx.x;
-    const int64_t i0 = (int64_t)blockIdx.x * kTile;
-    for (int t = tid; t < kTile * kTile; t += 4 * kTile) {
+    const int64_t i0 = (int64_t)blockIdx.x * kPanelRows;
+    for (int t = tid; t < kTile * kTile; t += 256) {
         const int kk = t / kTile, jj = t % kTile;                 // coalesced over jj
-        Ub[kk][quad_slot(jj)] = Uc[(k0 + kk) * n + k0 + jj];
+        Ub[kk][row16_slot(jj)] = Uc[(k0 + kk) * n + k0 + jj];
     }
     if (tid < kTile) Db[tid] = D[k0 + tid];
-    const int rr = tid >> 2, q = tid & 3;
+    const int rr = tid >> 4, q = tid & 15;
     const int64_t i = i0 + rr;
-    double v[16];
+    double v[4];
     if (i < k0) {
 #pragma unroll
-        for (int m = 0; m < 16; ++m) v[m] = Uc[(k0 + 4 * m + q) * n + i];
+        for (int m = 0; m < 4; ++m) v[m] = Uc[(k0 + 16 * m + q) * n + i];
     }
     __syncthreads();
-    if (i >= k0) return;                     // whole quads; rows share nothing
-    const double* Up = &Ub[0][16 * q];
+    if (i >= k0) return;                     // whole lane rows; rows share nothing
+    const double* Up = &Ub[0][4 * q];
     auto step = [&](auto kc) {
-        constexpr int kk = kTile - 1 - decltype(kc)::value, qk = kk & 3, mk = kk >> 2;
+        constexpr int kk = kTile - 1 - decltype(kc)::value, qk = kk & 15, mk = kk >> 4;
         const double dk = Db[kk];
-        const double u = quad_bcast<qk>(v[mk]) / dk;
-        Uc[(k0 + kk) * n + i] = u;           // the quad's four lanes store the same value
+        const double u = row_bcast<qk>(v[mk]) / dk;
+        Uc[(k0 + kk) * n + i] = u;           // the row's lanes store the same value
 #pragma unroll
-        for (int m = 0; m < 16; ++m) {
-            if (4 * m < kk) {                // some lane of the quad holds a column before kk
+        for (int m = 0; m < 4; ++m) {
+            if (16 * m < kk) {               // some lane of the row holds a column before kk
                 const double nv = v[m] - (u * Up[kk * kTile + m]) * dk;
-                v[m] = (4 * m + 3 < kk || q < kk - 4 * m) ? nv : v[m];
+                v[m] = (16 * m + 15 < kk || q < kk - 16 * m) ? nv : v[m];
             }
         }
     };
@@ -695,7 +709,7 @@ int run_ldlq(const void* wv, int64_t rows, int64_t n, int block, const double* H
     // beside the rest of the trailing update (look-ahead)
     hipLaunchKernelGGL(factor_diag_kernel, dim3(1), dim3(4 * kTile), 0, st, Uc, D, n, n - kTile, status);
     for (int64_t k0 = n - kTile; k0 > 0; k0 -= kTile) {
-        hipLaunchKernelGGL(factor_panel_kernel, dim3(blocks_for(k0, kTile)), dim3(4 * kTile), 0, st, Uc, D,
+        hipLaunchKernelGGL(factor_panel_kernel, dim3(blocks_for(k0, kPanelRows)), dim3(256), 0, st, Uc, D,
                            n, k0);
         const int64_t nb = k0 / kTile - 1;                         // the next block's tile column
         hipLaunchKernelGGL(factor_trailing_kernel<2>, dim3(2, (unsigned)(2 * (nb + 1))), dim3(256), 0, st, Uc,
