@@ -94,31 +94,38 @@ __global__ __launch_bounds__(256) void diag_kernel(const double* __restrict__ H,
 }
 
 // perm[rank(i)] = i, rank = number of columns with a larger diagonal, or an equal one and a
-// smaller index (a stable descending order).  64 columns i per workgroup; each wave counts over
-// a quarter of every 1024-value chunk of the diagonal staged in LDS (one value per step, read
-// by the wave's lanes alike), and the four counts are added.
-__global__ __launch_bounds__(256) void order_kernel(const double* __restrict__ diag, int64_t n,
-                                                    int* __restrict__ perm) {
-    __shared__ double chunk[1024];
-    __shared__ int part_rank[4][64];
+// smaller index (a stable descending order).  64 columns i per workgroup; each of its 16 waves
+// counts over a sixteenth of every 1024-value chunk of the diagonal staged in LDS (one value per
+// step, read by the wave's lanes alike), and the sixteen counts are added.
+constexpr int kOrderParts = 16;
+__global__ __launch_bounds__(64 * kOrderParts) void order_kernel(const double* __restrict__ diag, int64_t n,
+                                                                 int* __restrict__ perm) {
+    constexpr int kChunk = 1024, kPer = kChunk / kOrderParts;
+    __shared__ double chunk[kChunk];
+    __shared__ int part_rank[kOrderParts][64];
     const int il = threadIdx.x & 63, part = threadIdx.x >> 6;
     const int64_t i = (int64_t)blockIdx.x * 64 + il;
     const double d = i < n ? diag[i] : 0.0;
     int rank = 0;
-    for (int64_t c0 = 0; c0 < n; c0 += 1024) {
+    for (int64_t c0 = 0; c0 < n; c0 += kChunk) {
         __syncthreads();                                          // the previous chunk is used
-        for (int t = threadIdx.x; t < 1024; t += 256) chunk[t] = c0 + t < n ? diag[c0 + t] : 0.0;
+        chunk[threadIdx.x] = c0 + threadIdx.x < n ? diag[c0 + threadIdx.x] : 0.0;
         __syncthreads();
-        const int64_t jb = c0 + part * 256;
-        const int m = (int)(n - jb < 256 ? (n - jb > 0 ? n - jb : 0) : 256);
+        const int64_t jb = c0 + part * kPer;
+        const int m = (int)(n - jb < kPer ? (n - jb > 0 ? n - jb : 0) : kPer);
+#pragma unroll 8
         for (int jj = 0; jj < m; ++jj) {
-            const double e = chunk[part * 256 + jj];
+            const double e = chunk[part * kPer + jj];
             rank += (e > d || (e == d && jb + jj < i)) ? 1 : 0;
         }
     }
     part_rank[part][il] = rank;
     __syncthreads();
-    if (part == 0 && i < n) perm[part_rank[0][il] + part_rank[1][il] + part_rank[2][il] + part_rank[3][il]] = (int)i;
+    if (part == 0 && i < n) {
+        int r = 0;
+        for (int k = 0; k < kOrderParts; ++k) r += part_rank[k][il];
+        perm[r] = (int)i;
+    }
 }
 
 // lambda = damp * (sum of the diagonal in index order) / n: one wave stages the diagonal in
@@ -133,6 +140,7 @@ __global__ __launch_bounds__(64) void damping_kernel(const double* __restrict__ 
         __syncthreads();
         if (threadIdx.x == 0) {
             const int m = (int)(n - c0 < 1024 ? n - c0 : 1024);
+#pragma unroll 16
             for (int k = 0; k < m; ++k) tr += buf[k];
         }
     }
@@ -699,7 +707,7 @@ int run_ldlq(const void* wv, int64_t rows, int64_t n, int block, const double* H
 
     hipLaunchKernelGGL(clear_status_kernel, dim3(1), dim3(1), 0, st, status);
     hipLaunchKernelGGL(diag_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, H, n, diag);
-    hipLaunchKernelGGL(order_kernel, dim3(blocks_for(n, 64)), dim3(256), 0, st, diag, n, perm);
+    hipLaunchKernelGGL(order_kernel, dim3(blocks_for(n, 64)), dim3(64 * kOrderParts), 0, st, diag, n, perm);
     hipLaunchKernelGGL(damping_kernel, dim3(1), dim3(64), 0, st, diag, n, damp, lambda);
     if (hipGetLastError() != hipSuccess) return NVFP4_ERR_HIP;
     hipLaunchKernelGGL(init_a_kernel, dim3(blocks_for(n * n, 256)), dim3(256), 0, st, H, perm, lambda,
