@@ -148,8 +148,9 @@ __global__ __launch_bounds__(64) void damping_kernel(const double* __restrict__ 
 }
 
 // ---- factor: blocked, from the last 64-column block backwards ---------------------------
-// Uc holds A = Hp column-major (Uc[j n + i] = A_ij for i <= j) and is overwritten in place by
-// U.  Element (i, j) must receive its terms k = n-1, n-2, ..., j+1 in that order; the blocks
+// Uc holds A = Hp column-major (Uc[j n + i] = A_ij for i <= j; the lower triangle is never
+// written, and the values the kernels read from it feed only results they discard) and is
+// overwritten in place by U.  Element (i, j) must receive its terms k = n-1, n-2, ..., j+1 in that order; the blocks
 // are finished last-first and every kernel walks k downwards, so it does.
 
 __global__ __launch_bounds__(256) void init_a_kernel(const double* __restrict__ H,
@@ -159,6 +160,7 @@ __global__ __launch_bounds__(256) void init_a_kernel(const double* __restrict__ 
     const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (t >= n * n) return;
     const int64_t j = t / n, i = t % n;
+    if (i > j) return;                       // only the upper triangle is ever read as A
     double v = H[(int64_t)perm[i] * n + perm[j]];
     if (i == j) v = v + lambda[0];
     Uc[t] = v;
