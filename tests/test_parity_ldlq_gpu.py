@@ -62,6 +62,37 @@ def test_ldlq_parity_many_tiles_every_row(nv, rows, cols):
     check(nv, w, H)
 
 
+def test_ldlq_workspace_contents_do_not_matter(nv):
+    """The C call on a caller workspace filled with NaN, then reused for a second problem: only
+    the upper triangle of the permuted Hessian is written and read as A, and whatever the
+    kernels read elsewhere in the workspace feeds only discarded values, so both calls match
+    the oracle."""
+    import ctypes
+    rows, cols, block = 40, 256, 16
+    nbytes = nv.nvfp4_ldlq_workspace_bytes(rows, cols)
+    ws = torch.full((nbytes // 8,), float("nan"), dtype=torch.float64, device=DEV)
+    for seed in (66, 67):
+        g = workloads.generator(DEV, seed)
+        w = workloads.llm_weight(rows, cols, g, DEV).to(torch.bfloat16)
+        H = synthetic_hessian(cols, 2 * cols, seed)
+        _, sc, S = nv.quantize(w, "scalesweep_wmse", block, weight=torch.diagonal(H).float().contiguous())
+        q = torch.empty((rows, cols // 2), dtype=torch.uint8, device=DEV)
+        status = torch.zeros(1, dtype=torch.int32, device=DEV)
+        stream = ctypes.c_void_p(torch.cuda.current_stream(DEV).cuda_stream)
+        rc = nv.nvfp4_ldlq(ctypes.c_void_p(w.data_ptr()), 1, rows, cols, block,
+                           ctypes.c_void_p(H.data_ptr()), ctypes.c_void_p(sc.data_ptr()),
+                           ctypes.c_void_p(S.data_ptr()), ctypes.c_double(0.01),
+                           ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(status.data_ptr()),
+                           ctypes.c_void_p(ws.data_ptr()), nbytes, stream)
+        assert rc == 0
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0
+        q_ref = oracle.ldlq(workloads.host_array(w), H.cpu().numpy(), sc.cpu().numpy(),
+                            float(S.item()), block, 0.01)
+        got = q.cpu().numpy()
+        assert np.array_equal(got, q_ref), describe_mismatch(got, q_ref, "nibbles")
+
+
 @pytest.mark.parametrize("method,block", [("absmax", 16), ("four_over_six", 32),
                                           ("scalesweep_mse", 64), ("scalesweep_wmse", 128)])
 def test_ldlq_parity_methods_and_blocks(nv, method, block):
