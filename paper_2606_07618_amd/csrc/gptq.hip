@@ -329,26 +329,36 @@ __global__ __launch_bounds__(256) void factor_panel_kernel(double* __restrict__ 
 // chain per lane.
 constexpr int kHalf = kTile / 2;
 template <int R>
-struct FTrailLdsT {
-    double Ui[16 * R][kHalf + 1];  // Ui[ii][kk] = U_{i0+ii, k0+h+kk}
-    double Uj[16 * R][kHalf + 1];
+struct alignas(16) FTrailLdsT {
+    double Ui[kHalf][16 * R + 2];  // Ui[kk][ii] = U_{i0+ii, k0+h+kk} (rows padded: 16-byte rows)
+    double Uj[kHalf][16 * R + 2];
     double Dk[kTile];
 };
 using FTrailLds = FTrailLdsT<4>;
 
+// Lane (tr, tc) owns rows i0 + R tr .. + R - 1 and columns j0 + R tc .. + R - 1, so that its
+// values of a column and its operands of a step sit in 16-byte pairs.
 template <int R>
 __device__ __forceinline__ void factor_trailing_body(double* __restrict__ Uc, const double* __restrict__ D,
                                                      int64_t n, int64_t k0, int64_t i0, int64_t j0,
                                                      FTrailLdsT<R>& L) {
+    static_assert(R % 2 == 0, "pairs of values");
     constexpr int B = 16 * R;
     if (i0 > j0 + B - 1) return;
     if (threadIdx.x < kTile) L.Dk[threadIdx.x] = D[k0 + threadIdx.x];
     const int tr = threadIdx.x / 16, tc = threadIdx.x % 16;
-    double acc[R][R];
+    const int64_t ir = i0 + R * tr, jc = j0 + R * tc;
+    double acc[R][R];                        // acc[a][b]: (ir + a, jc + b)
 #pragma unroll
-    for (int a = 0; a < R; ++a)
+    for (int b = 0; b < R; ++b) {
+        const double2* src = reinterpret_cast<const double2*>(Uc + (jc + b) * n + ir);
 #pragma unroll
-        for (int b = 0; b < R; ++b) acc[a][b] = Uc[(j0 + tc + 16 * b) * n + i0 + tr + 16 * a];
+        for (int a = 0; a < R; a += 2) {
+            const double2 v = src[a / 2];
+            acc[a][b] = v.x;
+            acc[a + 1][b] = v.y;
+        }
+    }
     // each half's operands are loaded into registers while the previous half is computed
     constexpr int kPer = B * kHalf / 256;
     double pi[kPer], pj[kPer];
@@ -363,8 +373,8 @@ __device__ __forceinline__ void factor_trailing_body(double* __restrict__ Uc, co
 #pragma unroll
         for (int e = 0; e < kPer; ++e) {
             const int t = threadIdx.x + 256 * e, kk = t / B, r = t % B;
-            L.Ui[r][kk] = pi[e];
-            L.Uj[r][kk] = pj[e];
+            L.Ui[kk][r] = pi[e];
+            L.Uj[kk][r] = pj[e];
         }
         __syncthreads();
         if (h > 0) {
@@ -378,10 +388,16 @@ __device__ __forceinline__ void factor_trailing_body(double* __restrict__ Uc, co
 #pragma unroll(R == 2 ? 4 : 2)
         for (int kk = kHalf - 1; kk >= 0; --kk) {
             double ua[R], ub[R];
+            const double2* ap = reinterpret_cast<const double2*>(&L.Ui[kk][R * tr]);
+            const double2* bp = reinterpret_cast<const double2*>(&L.Uj[kk][R * tc]);
 #pragma unroll
-            for (int a = 0; a < R; ++a) ua[a] = L.Ui[tr + 16 * a][kk];
-#pragma unroll
-            for (int b = 0; b < R; ++b) ub[b] = L.Uj[tc + 16 * b][kk];
+            for (int a = 0; a < R; a += 2) {
+                const double2 av = ap[a / 2], bv = bp[a / 2];
+                ua[a] = av.x;
+                ua[a + 1] = av.y;
+                ub[a] = bv.x;
+                ub[a + 1] = bv.y;
+            }
             const double dk = L.Dk[h + kk];
 #pragma unroll
             for (int a = 0; a < R; ++a)
@@ -390,10 +406,10 @@ __device__ __forceinline__ void factor_trailing_body(double* __restrict__ Uc, co
         }
     }
 #pragma unroll
-    for (int a = 0; a < R; ++a)
+    for (int b = 0; b < R; ++b)
 #pragma unroll
-        for (int b = 0; b < R; ++b) {
-            const int64_t i = i0 + tr + 16 * a, j = j0 + tc + 16 * b;
+        for (int a = 0; a < R; ++a) {
+            const int64_t i = ir + a, j = jc + b;
             if (i <= j) Uc[j * n + i] = acc[a][b];
         }
 }
